@@ -1,0 +1,221 @@
+"""Throughput of one batch super-tree verification step on one MI355X.
+
+A step is the whole hot path over one batch: echo_gate -> echo_build_tree_mask
+-> echo_tree_verify_attn -> echo_accept, on inputs already resident in HBM.
+The default workload is the Qwen3-235B-A22B-shaped layer at batch 128 (tree
+8x10, budget 256, 64 q / 4 kv heads, head_dim 128, prefixes 1024-8192).
+
+Prints one JSON line with the metric (verified tree nodes per second), the
+roofline of the main attention kernel (timed with HIP events on its stream)
+and the CPU oracle timed on a bounded sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+METRIC = "verified tree nodes/sec (gate+verify-attn+accept), % HBM / MFMA peak"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def attn_algorithmic(batch, res, cfg):
+    """Algorithmic HBM bytes and FLOPs of one attention call."""
+    import numpy as np
+    qo = res["q_offsets"]
+    P = batch["prefix_len"].astype(np.int64)
+    n = np.diff(qo).astype(np.int64)
+    nq = int(qo[-1])
+    D, hq, hkv = cfg.head_dim, cfg.hq, cfg.hkv
+    kv_bytes = 4 * hkv * D * int(P.sum())                 # prefix K + V, bf16
+    row_bytes = nq * (2 * hq * D + 4 * hkv * D + 4 * hq * D + 4 * hq)  # q, k/v_new, out, lse
+    # visible keys per slot: prefix + ancestors-or-self (popcount of its mask row)
+    mask = res["tree_mask"][:nq]
+    anc = np.unpackbits(mask.view(np.uint8), axis=1).sum(axis=1).astype(np.int64)
+    slot_req = np.repeat(np.arange(cfg.R), n)
+    keys = P[slot_req] + anc
+    flops = 4 * D * hq * int(keys.sum())
+    return kv_bytes + row_bytes, flops
+
+
+def traffic_from_profile(attn_src_hash):
+    """HBM bytes per attention-kernel launch from the committed rocprofv3 PMC summary."""
+    path = os.path.join(ROOT, "profiles", "attn_main_q235b_pmc.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("attn_src_sha256") != attn_src_hash:
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(batch, cfg, budget_s=12.0):
+    """The oracle as written, single-threaded, on a bounded sample of the workload."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    import synth
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        g = oracle.gate(batch["cand_offsets"], batch["parent"], batch["logq"], cfg.budget)
+        m = oracle.build_tree_mask(batch["cand_offsets"], batch["parent"], batch["token"],
+                                   g["selected"], batch["root_token"], batch["prefix_len"],
+                                   cfg.budget, cfg.mask_words)
+        tgt = synth.target_for_slots(batch, m["q_offsets"], m["slot_cand"])
+        oracle.accept(m["q_offsets"], m["slot_parent"], m["slot_token"], tgt, 16)
+        t_front = time.perf_counter() - t0
+        qo = m["q_offsets"]
+        P = batch["prefix_len"].astype(np.int64)
+        n = np.diff(qo)
+        work_all = float((P * n).sum())
+        order = np.random.default_rng(0).permutation(cfg.R)
+        done_work, t_attn, used = 0.0, 0.0, []
+        for r in order:
+            rows = list(range(int(qo[r]), int(qo[r + 1])))
+            t1 = time.perf_counter()
+            oracle.tree_verify_attn(batch["q"], batch["k_new"], batch["v_new"], batch["k_cache"],
+                                    batch["v_cache"], batch["kv_offsets"], qo, m["tree_mask"],
+                                    cfg.hq, cfg.hkv, batch["sm_scale"], rows=rows)
+            t_attn += time.perf_counter() - t1
+            done_work += float(P[r] * n[r])
+            used.append(int(r))
+            if t_front + t_attn >= budget_s:
+                break
+    nq = int(qo[-1])
+    est = t_front + t_attn * work_all / max(done_work, 1.0)
+    return {
+        "value": nq / est, "unit": "verified tree nodes/sec", "cores": 1, "kind": "oracle",
+        "sample": (f"oracle gate+mask+accept on the full batch ({t_front:.2f} s) and float64 "
+                   f"attention for {len(used)} of {cfg.R} requests ({t_attn:.2f} s, "
+                   f"{100.0 * done_work / work_all:.1f}% of the prefix-key work), attention time "
+                   f"scaled by prefix-key work to the whole step ({est:.1f} s)"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="q235b")
+    ap.add_argument("--seed", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no "
+              "multi-GPU path: the verification step runs on a single MI355X.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2604_09603_amd as pkg
+    from paper_2604_09603_amd.step import VerifyStep
+
+    cfg = synth.CONFIGS[args.config]
+    log(f"generating {args.config} seed={args.seed}")
+    t0 = time.time()
+    batch = synth.make_batch(args.config, args.seed)
+    log(f"generated in {time.time() - t0:.1f} s; uploading")
+    st = VerifyStep(batch, device="cuda:0")
+    # the target model's argmax per slot is a stand-in input: gather it once for this batch
+    st.gate()
+    st.mask()
+    torch.cuda.synchronize()
+    res0 = st.fetch()
+    st.set_target(synth.target_for_slots(batch, res0["q_offsets"], res0["slot_cand"]))
+    torch.cuda.synchronize()
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        st.run()
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(args.steps):
+        pkg.set_attn_profile_events(ev_a[i], ev_b[i])
+        st.run()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    pkg.set_attn_profile_events(None, None)
+    ms_total = t_start.elapsed_time(t_end)
+    ms_step = ms_total / args.steps
+    attn_ms = [a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]
+    attn_us = 1000.0 * float(np.mean(attn_ms))
+
+    res = st.fetch()
+    if res["status"] != 0:
+        log(f"WARNING: data status bits {res['status']:#x}")
+    nq = res["num_slots"]
+    value = nq / (ms_step / 1000.0)
+    bytes_alg, flops_alg = attn_algorithmic(batch, res, cfg)
+    achieved_gbs = bytes_alg / (attn_us * 1e-6) / 1e9
+    with open(os.path.join(ROOT, "paper_2604_09603_amd", "csrc", "attn.hip"), "rb") as f:
+        attn_hash = hashlib.sha256(f.read()).hexdigest()
+    traffic = traffic_from_profile(attn_hash)
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "verified tree nodes/sec",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.config}: {synth.DESCRIPTION[args.config]}",
+            "batch": cfg.R, "budget": cfg.budget, "verified_slots": nq,
+            "draft_nodes": int(res["num_selected"]), "candidates": int(batch["cand_offsets"][-1]),
+            "kv_prefix_tokens": int(batch["kv_offsets"][-1]), "seed": args.seed,
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "kernel": "attn_main_kernel",
+            "bound": "hbm",
+            "achieved": achieved_gbs,
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": achieved_gbs / PEAK_HBM_GBS,
+            "traffic": traffic,
+            "algorithmic_bytes": bytes_alg,
+            "kernel_us": attn_us,
+            "tflops": flops_alg / (attn_us * 1e-6) / 1e12,
+            "mfma_frac": flops_alg / (attn_us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS,
+        },
+        "wall_s_timed": wall,
+        "mean_accept_len": float(np.mean(res["accept_len"])),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(batch, cfg)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

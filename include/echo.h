@@ -1,0 +1,194 @@
+/*
+ * echo.h -- C ABI of the batch super-tree verification library (MI355X / gfx950).
+ *
+ * One speculative-decoding step of a batch of R requests verifies a single
+ * "super-tree": the union of every request's draft candidates, under one
+ * batch-wide verification budget (the cap sum_i K_i <= K_max of eq. 4).  The
+ * four calls below are the four stages of that step:
+ *
+ *   echo_gate             path scores (eq. 5) and the global top-B selection
+ *   echo_build_tree_mask  flatten & pack of the selection (Fig. 3, stage 3)
+ *   echo_tree_verify_attn tree-masked GQA attention of every verify slot
+ *                         (the single verification forward, Section 3.1)
+ *   echo_accept           greedy acceptance of the longest matching path
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Every array argument is a DEVICE pointer owned by the caller.  The
+ *   library never allocates device memory: scratch space is the caller's
+ *   `workspace` (size from the matching *_workspace_size call, any
+ *   256-byte-aligned device buffer; contents on entry are ignored).
+ * - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *   stream), performs no host synchronisation and may be captured in a HIP
+ *   graph.  Calls on one stream run in order; the same workspace must not be
+ *   used by two calls that may run concurrently.
+ * - Return value: ECHO_OK, or a negative host-detected error, in which case
+ *   nothing was enqueued.
+ * - `status` (nullable device int32) receives the OR of ECHO_DATA_* bits for
+ *   problems found in the data itself.  The library ORs into it and never
+ *   clears it.  Data problems never abort: each is clamped as documented and
+ *   all outputs are still written.
+ * - Outputs sized by a capacity (R + budget verify slots) are written only
+ *   for the rows that exist (q_offsets[R]); later rows are left untouched.
+ * - bfloat16 tensors are passed as uint16_t bit patterns.
+ */
+#ifndef ECHO_H
+#define ECHO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef void* echo_stream_t; /* hipStream_t */
+
+/* ---- return codes ------------------------------------------------------ */
+#define ECHO_OK 0
+#define ECHO_ERR_INVALID_ARG (-1) /* null pointer, negative or inconsistent size  */
+#define ECHO_ERR_UNSUPPORTED (-2) /* head_dim != 128, limits below exceeded       */
+#define ECHO_ERR_WORKSPACE (-3)   /* workspace too small or misaligned            */
+#define ECHO_ERR_HIP (-4)         /* a HIP runtime call or kernel launch failed   */
+
+/* ---- data-error bits OR-ed into *status -------------------------------- */
+#define ECHO_DATA_NAN_LOGQ (1 << 0)        /* NaN log q: treated as -inf                    */
+#define ECHO_DATA_POS_LOGQ (1 << 1)        /* log q > 0: treated as 0                       */
+#define ECHO_DATA_BAD_PARENT (1 << 2)      /* parent not in [-1, local index): treated as -1 */
+#define ECHO_DATA_TOO_DEEP (1 << 3)        /* depth > ECHO_MAX_DEPTH: path score -inf       */
+#define ECHO_DATA_NOT_CLOSED (1 << 4)      /* selected node whose parent is not selected    */
+#define ECHO_DATA_OVER_CAPACITY (1 << 5)   /* more selected nodes than budget               */
+#define ECHO_DATA_BAD_SLOT_PARENT (1 << 6) /* slot_parent not in [0, slot)                  */
+#define ECHO_DATA_BAD_OFFSETS (1 << 7)     /* decreasing / out-of-capacity offsets          */
+
+/* ---- limits ------------------------------------------------------------ */
+#define ECHO_MAX_DEPTH 16       /* deepest draft node that can be selected           */
+#define ECHO_HEAD_DIM 128       /* the only supported head dimension                 */
+#define ECHO_MAX_BUDGET 16384   /* largest budget B                                  */
+#define ECHO_MAX_REQUESTS 4095  /* largest batch R                                   */
+
+/*
+ * echo_gate -- path scores and the global top-B selection.
+ *
+ * Path score (eq. 5): S_j = S_pa(j) + log q_j, S = 0 at the root, folded from
+ * the root towards the leaf with one IEEE binary32 add per level.  Selection
+ * (eq. 4 budget; Theorem 2 / Proposition 1 exchange argument): the
+ * min(budget, #finite S) candidates of the whole batch with the largest S;
+ * ties go to the smaller global candidate index; S = -inf is never selected.
+ * Because log q <= 0 the selection is closed under parents; a parallel pass
+ * checks every selected node's parent and sets ECHO_DATA_NOT_CLOSED if one is
+ * missing (impossible for data that passed the clamps below).
+ *
+ *   cand_offsets [R+1] int32   request-major CSR of candidates; g = cand_offsets[r] + n
+ *   parent       [N]   int32   request-local parent index, -1 = child of the root;
+ *                              must be < n (parents precede children)
+ *   logq         [N]   float   draft log-probability of the candidate token
+ *   budget                     B >= 0 draft nodes (<= ECHO_MAX_BUDGET)
+ *   path_score   [N]   float   (nullable) S per candidate after the clamps
+ *   selected     [N]   uint8   1 = verified this step, 0 = not
+ *   num_selected [1]   int32   min(budget, #finite S)
+ * Clamps: NaN log q -> -inf; log q > 0 -> 0; bad parent -> -1; depth >
+ * ECHO_MAX_DEPTH -> S = -inf.  N must equal cand_offsets[R] (not checked on
+ * the host: the offsets are device data).
+ */
+int32_t echo_gate(const int32_t* cand_offsets, const int32_t* parent, const float* logq,
+                  int32_t R, int32_t N, int32_t budget, float* path_score, uint8_t* selected,
+                  int32_t* num_selected, void* workspace, size_t workspace_bytes, int32_t* status,
+                  echo_stream_t stream);
+size_t echo_gate_workspace_size(int32_t R, int32_t N, int32_t budget);
+
+/*
+ * echo_build_tree_mask -- flatten & pack the selection into verify slots
+ * (Fig. 3, stage 3; the paper gives no layout, this is the library's).
+ *
+ * Request r owns slots [q_offsets[r], q_offsets[r+1]).  Local slot 0 is the
+ * root (the last verified token); local slots 1.. are the request's selected
+ * candidates in ascending global index, so a parent precedes its children.
+ *   q_offsets    [R+1]         int32  exclusive scan of 1 + #selected per request
+ *   slot_cand    [R+budget]    int32  global candidate index, -1 for a root
+ *   slot_parent  [R+budget]    int32  request-local parent slot, -1 for a root
+ *   slot_token   [R+budget]    int32  token[cand] or root_token[r]
+ *   position_ids [R+budget]    int32  prefix_len[r] + depth (root depth 0)
+ *   tree_mask    [R+budget][mask_words] uint32: bit j (word j>>5, bit j&31)
+ *                of row s is set iff local slot j is s or an ancestor of s
+ * mask_words must be >= ceil((budget+1)/32).  If more than `budget` nodes
+ * are selected only the first `budget` (ascending index) are packed
+ * (ECHO_DATA_OVER_CAPACITY).  A selected node whose parent is not selected
+ * hangs from its nearest selected ancestor (ECHO_DATA_NOT_CLOSED).
+ */
+int32_t echo_build_tree_mask(const int32_t* cand_offsets, const int32_t* parent,
+                             const int32_t* token, const uint8_t* selected,
+                             const int32_t* root_token, const int32_t* prefix_len, int32_t R,
+                             int32_t N, int32_t budget, int32_t* q_offsets, int32_t* slot_cand,
+                             int32_t* slot_parent, int32_t* slot_token, int32_t* position_ids,
+                             uint32_t* tree_mask, int32_t mask_words, void* workspace,
+                             size_t workspace_bytes, int32_t* status, echo_stream_t stream);
+size_t echo_build_tree_mask_workspace_size(int32_t R, int32_t N, int32_t budget);
+
+/*
+ * echo_tree_verify_attn -- tree-masked grouped-query verification attention
+ * (the one parallel target forward over the flattened union, Section 3.1;
+ * the paper's "specialized operators for irregular batch shapes").
+ *
+ * Slot s of request r, query head h, uses key/value head h / (Hq/Hkv) and
+ * sees the request's KV prefix rows [kv_offsets[r], kv_offsets[r+1]) plus
+ * the new keys of its local slots j whose tree_mask bit is set.  Logits
+ * sm_scale * <q, k> in fp32, softmax, output sum p * v in fp32.
+ *   q        [max_rows][Hq][128]  bf16 (slot-indexed, RoPE already applied)
+ *   k_new, v_new [max_rows][Hkv][128] bf16 (K/V of the verify slots)
+ *   k_cache, v_cache [kv_rows][Hkv][128] bf16, token-major (request r's prefix
+ *                                 is rows [kv_offsets[r], kv_offsets[r+1]))
+ *   kv_offsets [R+1] int64, q_offsets [R+1] int32, tree_mask as above
+ *   out      [max_rows][Hq][128]  float
+ *   lse      [max_rows][Hq]       float (nullable), natural log; -inf with out = 0
+ *                                 for a row that sees no key
+ * Requests with decreasing offsets, q_offsets beyond max_rows or kv_offsets
+ * outside [0, kv_rows] are skipped (ECHO_DATA_BAD_OFFSETS); their rows are
+ * not written.  Deterministic: no floating-point atomics.
+ */
+int32_t echo_tree_verify_attn(const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
+                              const uint16_t* k_cache, const uint16_t* v_cache,
+                              const int64_t* kv_offsets, int64_t kv_rows, const int32_t* q_offsets,
+                              const uint32_t* tree_mask, int32_t mask_words, int32_t R,
+                              int32_t max_rows, int32_t num_q_heads, int32_t num_kv_heads,
+                              int32_t head_dim, float sm_scale, float* out, float* lse,
+                              void* workspace, size_t workspace_bytes, int32_t* status,
+                              echo_stream_t stream);
+size_t echo_tree_verify_attn_workspace_size(int32_t R, int32_t max_rows, int32_t num_q_heads,
+                                            int32_t num_kv_heads, int32_t head_dim);
+
+/*
+ * echo_accept -- greedy acceptance (Section 2 standard SD, greedy decoding).
+ *
+ * Root slot valid; slot s valid iff its parent is valid, its depth <=
+ * max_depth and slot_token[s] == target_token[parent slot].  The path ends at
+ * the deepest valid slot (ties: smallest local slot).
+ *   target_token [max_rows] int32  target argmax after each slot
+ *   accept_len   [R]        int32  depth of the end slot (0..max_depth)
+ *   accept_slots [R][max_depth] int32 global slot indices of the accepted
+ *                           path from depth 1 to the end slot, -1 padded
+ *   bonus_token  [R]        int32  target_token[end slot] (-1 if no slots)
+ * max_depth in [1, ECHO_MAX_DEPTH].
+ */
+int32_t echo_accept(const int32_t* q_offsets, const int32_t* slot_parent,
+                    const int32_t* slot_token, const int32_t* target_token, int32_t R,
+                    int32_t max_rows, int32_t max_depth, int32_t* accept_len,
+                    int32_t* accept_slots, int32_t* bonus_token, int32_t* status,
+                    echo_stream_t stream);
+
+/*
+ * echo_set_attn_profile_events -- measurement hook (not a step of the method).
+ * While both events (hipEvent_t) are non-null, every echo_tree_verify_attn
+ * call records `start` on its stream right before its main attention kernel
+ * and `stop` right after it, so that a harness can time that kernel alone.
+ * NULL, NULL switches it off.  Process-wide setting, not thread-safe.
+ */
+int32_t echo_set_attn_profile_events(void* start, void* stop);
+
+const char* echo_status_string(int32_t code);
+const char* echo_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ECHO_H */

@@ -51,7 +51,7 @@ def tree_verify_attn(q, k_new, v_new, k_cache, v_cache, kv_offsets, q_offsets, t
     for r in range(R):
         q0, q1 = int(qo[r]), int(qo[r + 1])
         k0, k1 = int(ko[r]), int(ko[r + 1])
-        if q1 < q0 or q0 < 0 or q1 > cap or k1 < k0:
+        if q1 < q0 or q0 < 0 or q1 > cap or k0 < 0 or k1 < k0 or k1 > k_cache.shape[0]:
             status |= st.BAD_OFFSETS
             continue
         n = q1 - q0

@@ -1,0 +1,180 @@
+"""MI355X (gfx950) batch super-tree verification: Python binding of libecho.
+
+The four calls of one verification step live in ``libecho.so`` (HIP kernels
+behind a C ABI, declared in ``include/echo.h``).  This module only marshals
+arguments: torch device tensors are passed as raw pointers together with the
+current HIP stream.  There is no CPU fallback: if the library is missing or
+cannot be loaded every call raises.
+"""
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libecho.so")
+
+OK = 0
+ERR_INVALID_ARG = -1
+ERR_UNSUPPORTED = -2
+ERR_WORKSPACE = -3
+ERR_HIP = -4
+
+DATA_NAN_LOGQ = 1 << 0
+DATA_POS_LOGQ = 1 << 1
+DATA_BAD_PARENT = 1 << 2
+DATA_TOO_DEEP = 1 << 3
+DATA_NOT_CLOSED = 1 << 4
+DATA_OVER_CAPACITY = 1 << 5
+DATA_BAD_SLOT_PARENT = 1 << 6
+DATA_BAD_OFFSETS = 1 << 7
+
+MAX_DEPTH = 16
+HEAD_DIM = 128
+
+EXPORTS = [
+    "echo_gate", "echo_gate_workspace_size",
+    "echo_build_tree_mask", "echo_build_tree_mask_workspace_size",
+    "echo_tree_verify_attn", "echo_tree_verify_attn_workspace_size",
+    "echo_accept", "echo_set_attn_profile_events", "echo_status_string", "echo_version",
+]
+
+_lib = None
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_SZ = ctypes.c_size_t
+_F32 = ctypes.c_float
+
+_SIGS = {
+    "echo_gate": (_I32, [_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _SZ, _P, _P]),
+    "echo_gate_workspace_size": (_SZ, [_I32, _I32, _I32]),
+    "echo_build_tree_mask": (_I32, [_P, _P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P,
+                                    _I32, _P, _SZ, _P, _P]),
+    "echo_build_tree_mask_workspace_size": (_SZ, [_I32, _I32, _I32]),
+    "echo_tree_verify_attn": (_I32, [_P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _I32, _I32, _I32,
+                                     _I32, _I32, _F32, _P, _P, _P, _SZ, _P, _P]),
+    "echo_tree_verify_attn_workspace_size": (_SZ, [_I32, _I32, _I32, _I32, _I32]),
+    "echo_accept": (_I32, [_P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P]),
+    "echo_set_attn_profile_events": (_I32, [_P, _P]),
+    "echo_status_string": (ctypes.c_char_p, [_I32]),
+    "echo_version": (ctypes.c_char_p, []),
+}
+
+
+class EchoError(RuntimeError):
+    pass
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libecho (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise EchoError(f"{path} is missing: build it with "
+                        "`python -m paper_2604_09603_amd.build` (there is no CPU fallback)")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGS.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check(code: int, what: str):
+    if code != OK:
+        raise EchoError(f"{what}: {load().echo_status_string(code).decode()} ({code})")
+
+
+def set_attn_profile_events(start=None, stop=None):
+    """Measurement hook: record torch.cuda.Event objects around the main attention kernel."""
+    p = lambda e: None if e is None else ctypes.c_void_p(e.cuda_event)
+    _check(load().echo_set_attn_profile_events(p(start), p(stop)), "echo_set_attn_profile_events")
+
+
+def version() -> str:
+    return load().echo_version().decode()
+
+
+def status_string(code: int) -> str:
+    return load().echo_status_string(code).decode()
+
+
+def gate_workspace_size(R, N, budget) -> int:
+    return int(load().echo_gate_workspace_size(R, N, budget))
+
+
+def build_tree_mask_workspace_size(R, N, budget) -> int:
+    return int(load().echo_build_tree_mask_workspace_size(R, N, budget))
+
+
+def tree_verify_attn_workspace_size(R, max_rows, hq, hkv, head_dim=HEAD_DIM) -> int:
+    return int(load().echo_tree_verify_attn_workspace_size(R, max_rows, hq, hkv, head_dim))
+
+
+def echo_gate(cand_offsets, parent, logq, R, N, budget, path_score, selected, num_selected,
+              workspace, status=None, stream=None, check=True):
+    """Path scores and global top-B selection (eq. 5, eq. 4).  Device tensors."""
+    code = load().echo_gate(_ptr(cand_offsets), _ptr(parent), _ptr(logq), R, N, budget,
+                            _ptr(path_score), _ptr(selected), _ptr(num_selected), _ptr(workspace),
+                            workspace.numel() * workspace.element_size(), _ptr(status),
+                            _stream(stream))
+    if check:
+        _check(code, "echo_gate")
+    return code
+
+
+def echo_build_tree_mask(cand_offsets, parent, token, selected, root_token, prefix_len, R, N,
+                         budget, q_offsets, slot_cand, slot_parent, slot_token, position_ids,
+                         tree_mask, mask_words, workspace=None, status=None, stream=None,
+                         check=True):
+    """Flatten & pack the selection into verify slots.  Device tensors."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    code = load().echo_build_tree_mask(
+        _ptr(cand_offsets), _ptr(parent), _ptr(token), _ptr(selected), _ptr(root_token),
+        _ptr(prefix_len), R, N, budget, _ptr(q_offsets), _ptr(slot_cand), _ptr(slot_parent),
+        _ptr(slot_token), _ptr(position_ids), _ptr(tree_mask), mask_words, _ptr(workspace),
+        ws_bytes, _ptr(status), _stream(stream))
+    if check:
+        _check(code, "echo_build_tree_mask")
+    return code
+
+
+def echo_tree_verify_attn(q, k_new, v_new, k_cache, v_cache, kv_offsets, kv_rows, q_offsets,
+                          tree_mask, mask_words, R, max_rows, hq, hkv, head_dim, sm_scale, out,
+                          lse, workspace, status=None, stream=None, check=True):
+    """Tree-masked GQA verification attention.  bf16 inputs as int16/uint16/bfloat16 tensors."""
+    code = load().echo_tree_verify_attn(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(kv_offsets),
+        int(kv_rows), _ptr(q_offsets), _ptr(tree_mask), mask_words, R, max_rows, hq, hkv, head_dim,
+        float(sm_scale), _ptr(out), _ptr(lse), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(status), _stream(stream))
+    if check:
+        _check(code, "echo_tree_verify_attn")
+    return code
+
+
+def echo_accept(q_offsets, slot_parent, slot_token, target_token, R, max_rows, max_depth,
+                accept_len, accept_slots, bonus_token, status=None, stream=None, check=True):
+    """Greedy acceptance of the longest matching path per request."""
+    code = load().echo_accept(_ptr(q_offsets), _ptr(slot_parent), _ptr(slot_token),
+                              _ptr(target_token), R, max_rows, max_depth, _ptr(accept_len),
+                              _ptr(accept_slots), _ptr(bonus_token), _ptr(status),
+                              _stream(stream))
+    if check:
+        _check(code, "echo_accept")
+    return code

@@ -1,0 +1,180 @@
+// C ABI entry points: host-side argument checks, workspace sizing, launch.
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+#include <vector>
+
+#include "echo.h"
+#include "echo_internal.h"
+
+namespace echo {
+
+hipEvent_t g_attn_ev_start = nullptr;
+hipEvent_t g_attn_ev_stop = nullptr;
+
+int device_cu_count() {
+  static std::mutex mu;
+  static std::vector<int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  std::lock_guard<std::mutex> lock(mu);
+  if (dev >= int(cache.size())) cache.resize(dev + 1, 0);
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+}  // namespace echo
+
+namespace {
+inline bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+inline hipStream_t as_stream(echo_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
+}  // namespace
+
+extern "C" {
+
+size_t echo_gate_workspace_size(int32_t R, int32_t N, int32_t budget) {
+  if (R < 0 || N < 0 || budget < 0) return 0;
+  return echo::gate_workspace_bytes(R, N, budget);
+}
+
+int32_t echo_gate(const int32_t* cand_offsets, const int32_t* parent, const float* logq,
+                  int32_t R, int32_t N, int32_t budget, float* path_score, uint8_t* selected,
+                  int32_t* num_selected, void* workspace, size_t workspace_bytes, int32_t* status,
+                  echo_stream_t stream) {
+  if (R < 1 || N < 0 || budget < 0) return ECHO_ERR_INVALID_ARG;
+  if (R > ECHO_MAX_REQUESTS || budget > ECHO_MAX_BUDGET) return ECHO_ERR_UNSUPPORTED;
+  if (!cand_offsets || !num_selected || !workspace) return ECHO_ERR_INVALID_ARG;
+  if (N > 0 && (!parent || !logq || !selected)) return ECHO_ERR_INVALID_ARG;
+  if (!aligned256(workspace) || workspace_bytes < echo::gate_workspace_bytes(R, N, budget))
+    return ECHO_ERR_WORKSPACE;
+  return echo::launch_gate(cand_offsets, parent, logq, R, N, budget, path_score, selected,
+                           num_selected, workspace, status, as_stream(stream));
+}
+
+size_t echo_build_tree_mask_workspace_size(int32_t R, int32_t N, int32_t budget) {
+  (void)R;
+  (void)N;
+  (void)budget;
+  return 0;  // everything lives in LDS
+}
+
+int32_t echo_build_tree_mask(const int32_t* cand_offsets, const int32_t* parent,
+                             const int32_t* token, const uint8_t* selected,
+                             const int32_t* root_token, const int32_t* prefix_len, int32_t R,
+                             int32_t N, int32_t budget, int32_t* q_offsets, int32_t* slot_cand,
+                             int32_t* slot_parent, int32_t* slot_token, int32_t* position_ids,
+                             uint32_t* tree_mask, int32_t mask_words, void* workspace,
+                             size_t workspace_bytes, int32_t* status, echo_stream_t stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  if (R < 1 || N < 0 || budget < 0) return ECHO_ERR_INVALID_ARG;
+  if (R > ECHO_MAX_REQUESTS || budget > ECHO_MAX_BUDGET) return ECHO_ERR_UNSUPPORTED;
+  if (int64_t(mask_words) * 32 < int64_t(budget) + 1) return ECHO_ERR_INVALID_ARG;
+  if (!cand_offsets || !root_token || !prefix_len || !q_offsets || !slot_cand || !slot_parent ||
+      !slot_token || !position_ids || !tree_mask)
+    return ECHO_ERR_INVALID_ARG;
+  if (N > 0 && (!parent || !token || !selected)) return ECHO_ERR_INVALID_ARG;
+  if (echo::mask_lds_bytes(R, budget) > 150 * 1024) return ECHO_ERR_UNSUPPORTED;
+  return echo::launch_build_tree_mask(cand_offsets, parent, token, selected, root_token,
+                                      prefix_len, R, N, budget, q_offsets, slot_cand, slot_parent,
+                                      slot_token, position_ids, tree_mask, mask_words, status,
+                                      as_stream(stream));
+}
+
+size_t echo_tree_verify_attn_workspace_size(int32_t R, int32_t max_rows, int32_t num_q_heads,
+                                            int32_t num_kv_heads, int32_t head_dim) {
+  if (R < 1 || max_rows < 0 || num_q_heads < 1 || num_kv_heads < 1 || head_dim != ECHO_HEAD_DIM)
+    return 0;
+  return echo::attn_workspace_bytes(R, max_rows, num_q_heads, num_kv_heads);
+}
+
+int32_t echo_tree_verify_attn(const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
+                              const uint16_t* k_cache, const uint16_t* v_cache,
+                              const int64_t* kv_offsets, int64_t kv_rows,
+                              const int32_t* q_offsets, const uint32_t* tree_mask,
+                              int32_t mask_words, int32_t R, int32_t max_rows,
+                              int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                              float sm_scale, float* out, float* lse, void* workspace,
+                              size_t workspace_bytes, int32_t* status, echo_stream_t stream) {
+  if (R < 1 || max_rows < 0 || num_q_heads < 1 || num_kv_heads < 1 || mask_words < 1 ||
+      kv_rows < 0)
+    return ECHO_ERR_INVALID_ARG;
+  if (num_q_heads % num_kv_heads != 0) return ECHO_ERR_INVALID_ARG;
+  if (head_dim != ECHO_HEAD_DIM || R > ECHO_MAX_REQUESTS || kv_rows >= (int64_t(1) << 31))
+    return ECHO_ERR_UNSUPPORTED;
+  if (int64_t(max_rows) * num_q_heads >= (int64_t(1) << 26)) return ECHO_ERR_UNSUPPORTED;
+  if (!q || !k_new || !v_new || !kv_offsets || !q_offsets || !tree_mask || !out || !workspace)
+    return ECHO_ERR_INVALID_ARG;
+  if (kv_rows > 0 && (!k_cache || !v_cache)) return ECHO_ERR_INVALID_ARG;
+  if (!aligned256(workspace) ||
+      workspace_bytes < echo::attn_workspace_bytes(R, max_rows, num_q_heads, num_kv_heads))
+    return ECHO_ERR_WORKSPACE;
+  // 16-byte vector loads of every bf16 row
+  const uintptr_t mis = reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k_new) |
+                        reinterpret_cast<uintptr_t>(v_new) | reinterpret_cast<uintptr_t>(k_cache) |
+                        reinterpret_cast<uintptr_t>(v_cache) | reinterpret_cast<uintptr_t>(out);
+  if (mis & 15u) return ECHO_ERR_INVALID_ARG;
+  if (max_rows == 0) return ECHO_OK;
+  echo::AttnArgs a;
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.kv_offsets = kv_offsets;
+  a.kv_rows = kv_rows;
+  a.q_offsets = q_offsets;
+  a.tree_mask = tree_mask;
+  a.mask_words = mask_words;
+  a.R = R;
+  a.max_rows = max_rows;
+  a.hq = num_q_heads;
+  a.hkv = num_kv_heads;
+  a.sm_scale = sm_scale;
+  a.out = out;
+  a.lse = lse;
+  a.workspace = workspace;
+  a.status = status;
+  return echo::launch_tree_verify_attn(a, as_stream(stream));
+}
+
+int32_t echo_accept(const int32_t* q_offsets, const int32_t* slot_parent,
+                    const int32_t* slot_token, const int32_t* target_token, int32_t R,
+                    int32_t max_rows, int32_t max_depth, int32_t* accept_len,
+                    int32_t* accept_slots, int32_t* bonus_token, int32_t* status,
+                    echo_stream_t stream) {
+  if (R < 1 || max_rows < 0 || max_depth < 1) return ECHO_ERR_INVALID_ARG;
+  if (max_depth > ECHO_MAX_DEPTH || R > ECHO_MAX_REQUESTS) return ECHO_ERR_UNSUPPORTED;
+  if (!q_offsets || !accept_len || !accept_slots || !bonus_token) return ECHO_ERR_INVALID_ARG;
+  if (max_rows > 0 && (!slot_parent || !slot_token || !target_token)) return ECHO_ERR_INVALID_ARG;
+  return echo::launch_accept(q_offsets, slot_parent, slot_token, target_token, R, max_rows,
+                             max_depth, accept_len, accept_slots, bonus_token, status,
+                             as_stream(stream));
+}
+
+int32_t echo_set_attn_profile_events(void* start, void* stop) {
+  if ((start == nullptr) != (stop == nullptr)) return ECHO_ERR_INVALID_ARG;
+  echo::g_attn_ev_start = reinterpret_cast<hipEvent_t>(start);
+  echo::g_attn_ev_stop = reinterpret_cast<hipEvent_t>(stop);
+  return ECHO_OK;
+}
+
+const char* echo_status_string(int32_t code) {
+  switch (code) {
+    case ECHO_OK: return "ok";
+    case ECHO_ERR_INVALID_ARG: return "invalid argument";
+    case ECHO_ERR_UNSUPPORTED: return "unsupported size or shape";
+    case ECHO_ERR_WORKSPACE: return "workspace too small or not 256-byte aligned";
+    case ECHO_ERR_HIP: return "HIP launch or runtime failure";
+    default: return "unknown status";
+  }
+}
+
+const char* echo_version(void) { return "echo-mi355x 0.1.0 (gfx950)"; }
+
+}  // extern "C"

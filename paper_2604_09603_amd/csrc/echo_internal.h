@@ -1,0 +1,60 @@
+// Launchers behind the C ABI (one per stage).  Host code; arguments already validated.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace echo {
+
+int32_t launch_gate(const int32_t* cand_offsets, const int32_t* parent, const float* logq,
+                    int32_t R, int32_t N, int32_t budget, float* path_score, uint8_t* selected,
+                    int32_t* num_selected, void* workspace, int32_t* status, hipStream_t stream);
+size_t gate_workspace_bytes(int32_t R, int32_t N, int32_t budget);
+
+int32_t launch_build_tree_mask(const int32_t* cand_offsets, const int32_t* parent,
+                               const int32_t* token, const uint8_t* selected,
+                               const int32_t* root_token, const int32_t* prefix_len, int32_t R,
+                               int32_t N, int32_t budget, int32_t* q_offsets, int32_t* slot_cand,
+                               int32_t* slot_parent, int32_t* slot_token, int32_t* position_ids,
+                               uint32_t* tree_mask, int32_t mask_words, int32_t* status,
+                               hipStream_t stream);
+size_t mask_lds_bytes(int32_t R, int32_t budget);
+
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  const uint16_t* k_cache;
+  const uint16_t* v_cache;
+  const int64_t* kv_offsets;
+  int64_t kv_rows;
+  const int32_t* q_offsets;
+  const uint32_t* tree_mask;
+  int32_t mask_words;
+  int32_t R;
+  int32_t max_rows;
+  int32_t hq;
+  int32_t hkv;
+  float sm_scale;
+  float* out;
+  float* lse;
+  void* workspace;
+  int32_t* status;
+};
+int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream);
+size_t attn_workspace_bytes(int32_t R, int32_t max_rows, int32_t hq, int32_t hkv);
+
+int32_t launch_accept(const int32_t* q_offsets, const int32_t* slot_parent,
+                      const int32_t* slot_token, const int32_t* target_token, int32_t R,
+                      int32_t max_rows, int32_t max_depth, int32_t* accept_len,
+                      int32_t* accept_slots, int32_t* bonus_token, int32_t* status,
+                      hipStream_t stream);
+
+int device_cu_count();
+
+// measurement hook: events recorded around the main attention kernel (may be null)
+extern hipEvent_t g_attn_ev_start;
+extern hipEvent_t g_attn_ev_stop;
+
+}  // namespace echo

@@ -1,0 +1,127 @@
+"""Device-resident buffers for one verification step and the four calls in order.
+
+``VerifyStep`` owns every input, output and workspace of a batch on one GPU
+(torch allocations, used only as device memory) and enqueues echo_gate ->
+echo_build_tree_mask -> echo_tree_verify_attn -> echo_accept on the current
+stream.  The target argmax per verify slot is an input of the last stage; the
+caller supplies it (``set_target``) because it comes from the target model.
+"""
+import numpy as np
+import torch
+
+from . import (HEAD_DIM, MAX_DEPTH, echo_accept, echo_build_tree_mask, echo_gate,
+               echo_tree_verify_attn, gate_workspace_size, tree_verify_attn_workspace_size)
+
+
+def _aligned_workspace(nbytes, device):
+    raw = torch.empty(max(int(nbytes), 1) + 256, dtype=torch.uint8, device=device)
+    off = (-raw.data_ptr()) % 256
+    return raw[off:off + max(int(nbytes), 1)]
+
+
+def _dev(a, device, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.to(device)
+
+
+class VerifyStep:
+    def __init__(self, batch, device="cuda:0", max_depth=MAX_DEPTH):
+        cfg = batch["cfg"]
+        self.cfg = cfg
+        self.device = device
+        self.R = cfg.R
+        self.N = int(batch["cand_offsets"][-1])
+        self.B = cfg.budget
+        self.cap = cfg.R + cfg.budget
+        self.W = (cfg.budget + 1 + 31) // 32
+        self.hq, self.hkv, self.D = cfg.hq, cfg.hkv, cfg.head_dim
+        self.max_depth = max_depth
+        d = device
+        i16 = lambda a: _dev(np.asarray(a, np.uint16).view(np.int16), d)
+        # inputs
+        self.cand_offsets = _dev(batch["cand_offsets"].astype(np.int32), d)
+        self.parent = _dev(batch["parent"].astype(np.int32), d)
+        self.token = _dev(batch["token"].astype(np.int32), d)
+        self.logq = _dev(batch["logq"].astype(np.float32), d)
+        self.root_token = _dev(batch["root_token"].astype(np.int32), d)
+        self.prefix_len = _dev(batch["prefix_len"].astype(np.int32), d)
+        self.kv_offsets = _dev(batch["kv_offsets"].astype(np.int64), d)
+        self.kv_rows = int(batch["kv_offsets"][-1])
+        self.q = i16(batch["q"])
+        self.k_new = i16(batch["k_new"])
+        self.v_new = i16(batch["v_new"])
+        self.k_cache = i16(batch["k_cache"])
+        self.v_cache = i16(batch["v_cache"])
+        self.sm_scale = float(batch["sm_scale"])
+        # outputs
+        z32 = lambda *s: torch.zeros(s, dtype=torch.int32, device=d)
+        self.path_score = torch.zeros(max(self.N, 1), dtype=torch.float32, device=d)
+        self.selected = torch.zeros(max(self.N, 1), dtype=torch.uint8, device=d)
+        self.num_selected = z32(1)
+        self.q_offsets = z32(self.R + 1)
+        self.slot_cand = z32(self.cap)
+        self.slot_parent = z32(self.cap)
+        self.slot_token = z32(self.cap)
+        self.position_ids = z32(self.cap)
+        self.tree_mask = z32(self.cap, self.W)
+        self.out = torch.zeros((self.cap, self.hq, self.D), dtype=torch.float32, device=d)
+        self.lse = torch.zeros((self.cap, self.hq), dtype=torch.float32, device=d)
+        self.target_token = z32(self.cap)
+        self.accept_len = z32(self.R)
+        self.accept_slots = z32(self.R, max_depth)
+        self.bonus_token = z32(self.R)
+        self.status = z32(1)
+        self.gate_ws = _aligned_workspace(gate_workspace_size(self.R, self.N, self.B), d)
+        self.attn_ws = _aligned_workspace(
+            tree_verify_attn_workspace_size(self.R, self.cap, self.hq, self.hkv, self.D), d)
+
+    # ---- the four stages -------------------------------------------------
+    def gate(self, stream=None):
+        echo_gate(self.cand_offsets, self.parent, self.logq, self.R, self.N, self.B,
+                  self.path_score, self.selected, self.num_selected, self.gate_ws,
+                  status=self.status, stream=stream)
+
+    def mask(self, stream=None):
+        echo_build_tree_mask(self.cand_offsets, self.parent, self.token, self.selected,
+                             self.root_token, self.prefix_len, self.R, self.N, self.B,
+                             self.q_offsets, self.slot_cand, self.slot_parent, self.slot_token,
+                             self.position_ids, self.tree_mask, self.W, status=self.status,
+                             stream=stream)
+
+    def attn(self, stream=None):
+        echo_tree_verify_attn(self.q, self.k_new, self.v_new, self.k_cache, self.v_cache,
+                              self.kv_offsets, self.kv_rows, self.q_offsets, self.tree_mask,
+                              self.W, self.R, self.cap, self.hq, self.hkv, self.D, self.sm_scale,
+                              self.out, self.lse, self.attn_ws, status=self.status,
+                              stream=stream)
+
+    def accept(self, stream=None):
+        echo_accept(self.q_offsets, self.slot_parent, self.slot_token, self.target_token, self.R,
+                    self.cap, self.max_depth, self.accept_len, self.accept_slots,
+                    self.bonus_token, status=self.status, stream=stream)
+
+    def run(self, stream=None):
+        self.gate(stream)
+        self.mask(stream)
+        self.attn(stream)
+        self.accept(stream)
+
+    def set_target(self, target_per_slot):
+        t = np.zeros(self.cap, np.int32)
+        t[:len(target_per_slot)] = target_per_slot
+        self.target_token.copy_(torch.from_numpy(t))
+
+    def fetch(self):
+        torch.cuda.synchronize()
+        g = lambda t: t.cpu().numpy()
+        nq = int(self.q_offsets[-1].item())
+        return dict(
+            path_score=g(self.path_score)[:self.N], selected=g(self.selected)[:self.N],
+            num_selected=int(self.num_selected.item()), q_offsets=g(self.q_offsets),
+            slot_cand=g(self.slot_cand), slot_parent=g(self.slot_parent),
+            slot_token=g(self.slot_token), position_ids=g(self.position_ids),
+            tree_mask=g(self.tree_mask).view(np.uint32), out=g(self.out), lse=g(self.lse),
+            accept_len=g(self.accept_len), accept_slots=g(self.accept_slots),
+            bonus_token=g(self.bonus_token), status=int(self.status.item()), num_slots=nq)

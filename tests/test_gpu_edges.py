@@ -1,0 +1,134 @@
+"""GPU parity on small adversarial inputs: score ties, degenerate budgets, empty
+requests, empty prefixes, invalid data (status bits), deep chains, wide masks."""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests import gpu_common as gc
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu():
+    gc.require_gpu()
+
+
+def _bf16(rng, *shape):
+    return synth.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32))
+
+
+def make_micro_batch(pool, budget, hq=8, hkv=2, p_range=(0, 70), seed=0):
+    """Wrap a candidate pool into a full batch with random attention tensors."""
+    rng = np.random.default_rng(seed)
+    R = len(pool["cand_offsets"]) - 1
+    cfg = synth.Config("micro", R, 1, 1, 1.0, 8, budget, hq, hkv, 128, p_range[0], p_range[1],
+                       ("const", 1.0))
+    P = rng.integers(p_range[0], p_range[1] + 1, size=R).astype(np.int32)
+    kvo = np.zeros(R + 1, np.int64)
+    kvo[1:] = np.cumsum(P)
+    T = int(kvo[-1])
+    cap = R + budget
+    N = int(pool["cand_offsets"][-1])
+    b = dict(cfg=cfg, seed=seed, cand_offsets=pool["cand_offsets"].astype(np.int32),
+             parent=pool["parent"].astype(np.int32), token=pool["token"].astype(np.int32),
+             logq=pool["logq"].astype(np.float32), root_token=pool["root_token"].astype(np.int32),
+             target=rng.integers(0, 4, size=N).astype(np.int32),
+             root_target=rng.integers(0, 4, size=R).astype(np.int32),
+             prefix_len=P, kv_offsets=kvo, q=_bf16(rng, cap, hq, 128),
+             k_new=_bf16(rng, cap, hkv, 128), v_new=_bf16(rng, cap, hkv, 128),
+             k_cache=_bf16(rng, T, hkv, 128), v_cache=_bf16(rng, T, hkv, 128),
+             sm_scale=np.float32(1 / math.sqrt(128)))
+    return b
+
+
+def _front_ref(b, max_depth=16):
+    cfg = b["cfg"]
+    g = oracle.gate(b["cand_offsets"], b["parent"], b["logq"], cfg.budget)
+    m = oracle.build_tree_mask(b["cand_offsets"], b["parent"], b["token"], g["selected"],
+                               b["root_token"], b["prefix_len"], cfg.budget, cfg.mask_words)
+    tgt = synth.target_for_slots(b, m["q_offsets"], m["slot_cand"])
+    a = oracle.accept(m["q_offsets"], m["slot_parent"], m["slot_token"], tgt, max_depth)
+    return dict(gate=g, mask=m, target=tgt, accept=a,
+                status=g["status"] | m["status"] | a["status"])
+
+
+def _check_all(b, attention=True):
+    ref = _front_ref(b)
+    st, res = gc.run_gpu(b, ref["target"])
+    gc.compare_front(res, ref, int(b["cand_offsets"][-1]))
+    assert res["status"] == ref["status"], (res["status"], ref["status"])
+    if attention:
+        cfg = b["cfg"]
+        m = ref["mask"]
+        rows = list(range(m["num_slots"]))
+        ro, rl, _ = oracle.tree_verify_attn(b["q"], b["k_new"], b["v_new"], b["k_cache"],
+                                            b["v_cache"], b["kv_offsets"], m["q_offsets"],
+                                            m["tree_mask"], cfg.hq, cfg.hkv, b["sm_scale"])
+        gc.compare_attn(res["out"], res["lse"], ro, rl, rows)
+    return res, ref
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_micro_pools_with_ties(seed):
+    rng = np.random.default_rng(1000 + seed)
+    pool = synth.micro_pool(rng, int(rng.integers(1, 7)), int(rng.integers(0, 40)), vocab=4)
+    N = int(pool["cand_offsets"][-1])
+    budget = int(rng.choice([0, 1, 3, max(1, N // 3), N, N + 5]))
+    hq, hkv = [(8, 2), (4, 4), (16, 1), (6, 3)][seed % 4]
+    b = make_micro_batch(pool, budget, hq, hkv, p_range=(0, 150), seed=seed)
+    print(f"[edges] micro seed={seed} R={len(pool['cand_offsets']) - 1} N={N} B={budget}", flush=True)
+    _check_all(b)
+
+
+def test_invalid_data_sets_status_bits():
+    offs = np.array([0, 5, 9], np.int32)
+    parent = np.array([-1, 0, 7, 1, 2, -1, -5, 0, 2], np.int32)      # 7 and -5 are bad
+    logq = np.array([-0.5, np.nan, 0.25, -1.0, -0.5, -0.25, -0.5, -1.0, -2.0], np.float32)
+    pool = dict(cand_offsets=offs, parent=parent, token=np.arange(9, dtype=np.int32) % 4,
+                logq=logq, root_token=np.array([1, 2], np.int32))
+    b = make_micro_batch(pool, 6, p_range=(3, 9))
+    res, ref = _check_all(b)
+    assert (res["status"] & 7) == 7
+
+
+def test_deep_chain_and_wide_mask():
+    """A 20-deep chain (depth cap) plus 70 root children in another request (3 mask words)."""
+    p1 = np.array([-1] + list(range(19)), np.int32)
+    p2 = np.full(70, -1, np.int32)
+    pool = dict(cand_offsets=np.array([0, 20, 90], np.int32), parent=np.concatenate([p1, p2]),
+                token=np.zeros(90, np.int32), logq=np.full(90, -0.001, np.float32),
+                root_token=np.array([0, 0], np.int32))
+    b = make_micro_batch(pool, 80, hq=4, hkv=4, p_range=(0, 40))
+    res, ref = _check_all(b)
+    assert res["status"] & 8
+
+
+def test_all_equal_scores_large_tie_class():
+    """Thousands of candidates with identical path scores: ties resolved by index."""
+    rng = np.random.default_rng(5)
+    R, n = 6, 1500
+    offs = np.arange(R + 1, dtype=np.int32) * n
+    parent = np.concatenate([np.array([-1] * 40 + [int(rng.integers(0, 40)) for _ in range(n - 40)],
+                                      np.int32) for _ in range(R)])
+    pool = dict(cand_offsets=offs, parent=parent, token=np.zeros(R * n, np.int32),
+                logq=np.full(R * n, -0.5, np.float32), root_token=np.zeros(R, np.int32))
+    for budget in (100, 239, 240, 241, 5000):
+        b = make_micro_batch(pool, budget, hq=4, hkv=2, p_range=(10, 20))
+        _check_all(b, attention=(budget == 241))
+
+
+def test_empty_requests_and_prefixes():
+    offs = np.array([0, 0, 4, 4, 7], np.int32)            # requests 0 and 2 have no candidates
+    parent = np.array([-1, 0, 0, 1, -1, -1, 1], np.int32)
+    pool = dict(cand_offsets=offs, parent=parent, token=np.arange(7, dtype=np.int32) % 3,
+                logq=np.array([-0.1, -0.2, -0.3, -0.4, -0.1, -0.5, -0.2], np.float32),
+                root_token=np.array([0, 1, 2, 0], np.int32))
+    b = make_micro_batch(pool, 5, hq=8, hkv=4, p_range=(0, 0))    # no KV prefix at all
+    _check_all(b)
+    b = make_micro_batch(pool, 0, hq=8, hkv=4, p_range=(0, 300))  # budget 0: decode only
+    _check_all(b)

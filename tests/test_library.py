@@ -1,0 +1,53 @@
+"""The C-ABI library builds for gfx950, loads without a GPU and exports every declared symbol."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2604_09603_amd as pkg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "echo.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:int32_t|size_t|const char\*)\s+(echo_\w+)\(", text, re.M)))
+
+
+def test_header_and_binding_agree():
+    assert _declared() == sorted(pkg.EXPORTS)
+
+
+def test_library_exports_every_symbol():
+    if not os.path.exists(pkg.LIB_PATH):
+        pytest.skip("libecho.so not built (run __graft_entry__.build())")
+    lib = ctypes.CDLL(pkg.LIB_PATH)
+    for name in _declared():
+        assert hasattr(lib, name), name
+    lib = pkg.load()
+    assert "gfx950" in pkg.version()
+    assert pkg.status_string(pkg.ERR_WORKSPACE).startswith("workspace")
+
+
+def test_host_side_errors_need_no_gpu():
+    """Argument checks run on the host and return before touching the device."""
+    if not os.path.exists(pkg.LIB_PATH):
+        pytest.skip("libecho.so not built")
+    lib = pkg.load()
+    P = ctypes.c_void_p
+    # R = 0, negative budget, head_dim != 128, Hq % Hkv != 0, max_depth > 16
+    assert lib.echo_gate(None, None, None, 0, 0, 0, None, None, None, None, 0, None, None) == pkg.ERR_INVALID_ARG
+    assert lib.echo_gate(P(8), P(8), P(8), 1, 1, -1, None, P(8), P(8), P(256), 1 << 20, None, None) == pkg.ERR_INVALID_ARG
+    assert lib.echo_gate(P(256), P(256), P(256), 1, 1, 4, None, P(256), P(256), P(256), 0, None, None) == pkg.ERR_WORKSPACE
+    assert lib.echo_tree_verify_attn_workspace_size(4, 20, 8, 8, 64) == 0
+    assert lib.echo_tree_verify_attn(P(16), P(16), P(16), P(16), P(16), P(16), 10, P(16), P(16), 1,
+                                     1, 4, 6, 4, 128, 1.0, P(16), None, P(256), 1 << 30, None,
+                                     None) == pkg.ERR_INVALID_ARG
+    assert lib.echo_tree_verify_attn(P(16), P(16), P(16), P(16), P(16), P(16), 10, P(16), P(16), 1,
+                                     1, 4, 8, 8, 64, 1.0, P(16), None, P(256), 1 << 30, None,
+                                     None) == pkg.ERR_UNSUPPORTED
+    assert lib.echo_accept(P(8), P(8), P(8), P(8), 1, 4, 17, P(8), P(8), P(8), None, None) == pkg.ERR_UNSUPPORTED
+    assert lib.echo_build_tree_mask(P(8), P(8), P(8), P(8), P(8), P(8), 1, 1, 64, P(8), P(8), P(8),
+                                    P(8), P(8), P(8), 1, None, 0, None, None) == pkg.ERR_INVALID_ARG
