@@ -148,6 +148,9 @@ def main():
     ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
+    # torch only reads an event it has recorded itself: record each once, the library re-records
+    for e in ev_a + ev_b:
+        e.record(stream)
     log(f"timing {args.steps} steps")
     torch.cuda.synchronize()
     wall0 = time.perf_counter()

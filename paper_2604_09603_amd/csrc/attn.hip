@@ -26,11 +26,11 @@ namespace {
 constexpr int kD = ECHO_HEAD_DIM;   // 128
 constexpr int kThreads = 256;       // plan / combine workgroups
 constexpr int kWaves = kThreads / kWave;
-constexpr int kMainWaves = 4;       // main kernel: waves per workgroup
+constexpr int kMainWaves = 8;       // main kernel: waves per workgroup
 constexpr int kMT = 2;              // 16-row tiles per wave per row pass
+constexpr int kStages = 4;          // LDS ring depth (64-key K+V tiles)
+constexpr int kCombineRows = 8;     // rows per combine workgroup
 constexpr int kTileKeys = 64;       // keys staged in LDS per step
-constexpr int kRowBytes = kD * 2 + 16;  // padded LDS row (bf16), breaks bank conflicts
-constexpr int kRowHalfs = kRowBytes / 2;
 constexpr int kMaxParts = 16;       // chunks per pair at most
 constexpr int kChunkMin = 256;      // shortest chunk (keys)
 constexpr float kLog2e = 1.4426950408889634f;
@@ -53,9 +53,10 @@ struct PairInfo {
 };
 
 struct AttnWs {
-  int32_t* meta;     // [0] = number of items
+  int32_t* meta;     // [0] = number of items, [1] = number of combine groups
   Item* items;
   PairInfo* pairs;
+  int2* cgroups;     // (pair, first row) of each combine workgroup
   float* part_ml;    // [rows][2]: running max (log2 units), sum
   float* part_o;     // [rows][128]
 };
@@ -66,8 +67,12 @@ __host__ inline size_t item_capacity(int R, int hkv, int target_items) {
   return size_t(target_items) + size_t(R) * hkv;
 }
 
+__host__ inline size_t cgroup_capacity(int R, int max_rows, int hq, int hkv) {
+  return (size_t(max_rows) * hq + kCombineRows - 1) / kCombineRows + size_t(R) * hkv;
+}
+
 __host__ __device__ inline AttnWs attn_layout(void* base, int R, int hkv, size_t item_cap,
-                                              size_t part_rows) {
+                                              size_t cg_cap, size_t part_rows) {
   char* p = static_cast<char*>(base);
   AttnWs w;
   w.meta = reinterpret_cast<int32_t*>(p);
@@ -76,6 +81,8 @@ __host__ __device__ inline AttnWs attn_layout(void* base, int R, int hkv, size_t
   p += al(item_cap * sizeof(Item));
   w.pairs = reinterpret_cast<PairInfo*>(p);
   p += al(size_t(R) * hkv * sizeof(PairInfo));
+  w.cgroups = reinterpret_cast<int2*>(p);
+  p += al(cg_cap * sizeof(int2));
   w.part_ml = reinterpret_cast<float*>(p);
   p += al(part_rows * 2 * sizeof(float));
   w.part_o = reinterpret_cast<float*>(p);
@@ -110,8 +117,8 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
   ch = (ch + kTileKeys - 1) / kTileKeys * kTileKeys;
   if (ch < kChunkMin) ch = kChunkMin;
 
-  // pairs in request-major order; scan their item counts and partial rows
-  int item_run = 0, row_run = 0;
+  // pairs in request-major order; scan their item counts, partial rows, combine groups
+  int item_run = 0, row_run = 0, cg_run = 0;
   const int npairs = R * hkv;
   for (int base = 0; base < npairs; base += kThreads) {
     const int pr = base + tid;
@@ -140,9 +147,11 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
         nparts = int(np);
       }
     }
-    int tot_items, tot_rows;
+    int tot_items, tot_rows, tot_cg;
+    const int ncg = nparts > 0 ? (rows + kCombineRows - 1) / kCombineRows : 0;
     const int ib = item_run + block_exclusive_sum<kThreads>(nparts, s_scan, &tot_items);
     const int rb = row_run + block_exclusive_sum<kThreads>(nparts * rows, s_scan, &tot_rows);
+    const int cb = cg_run + block_exclusive_sum<kThreads>(ncg, s_scan, &tot_cg);
     if (pr < npairs) {
       PairInfo pi;
       pi.part_base = rb;
@@ -161,191 +170,243 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
         it.part = i | (i == nparts - 1 ? (1 << 30) : 0);
         ws.items[ib + i] = it;
       }
+      for (int c = 0; c < ncg; ++c) ws.cgroups[cb + c] = make_int2(pr, c * kCombineRows);
     }
     item_run += tot_items;
     row_run += tot_rows;
+    cg_run += tot_cg;
   }
-  if (tid == 0) ws.meta[0] = item_run;
+  if (tid == 0) {
+    ws.meta[0] = item_run;
+    ws.meta[1] = cg_run;
+  }
 }
 
 // ---------------------------------------------------------------- main ----
+// LDS tile layout: 64 key rows x 256 bytes per tensor, no padding.  The 16-byte
+// chunk c of row r is stored at chunk position c ^ (r & 15), so that 16 rows
+// read at the same logical column fall into 16 different bank groups.
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) shortx4 lds_shortx4_t;
+
+constexpr int kTileBytes = kTileKeys * kD * 2;  // 16 KB per tensor
+constexpr int kStageBytes = 2 * kTileBytes;     // K then V
+
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   __bf16 a = static_cast<__bf16>(lo);
   __bf16 b = static_cast<__bf16>(hi);
-  return uint32_t(__builtin_bit_cast(uint16_t, a)) | (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
+  return uint32_t(__builtin_bit_cast(uint16_t, a)) |
+         (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
 }
 
-// Stage keys [t0, t0 + kTileKeys) of one (K, V) source into LDS; rows >= tn are zero.
-// src row i lives at base + i * stride (bf16 elements).
-template <int NT>
-__device__ __forceinline__ void stage_tile(uint16_t* s_k, uint16_t* s_v, const uint16_t* kbase,
+__device__ __forceinline__ int swz(int row, int chunk) {
+  return row * 256 + ((chunk ^ (row & 15)) << 4);
+}
+
+// Direct HBM -> LDS copy of one 64-key tile of K and V (each lane moves 16 bytes
+// per instruction, 1 KB = 4 rows per wave instruction).  Rows >= tn re-read row
+// tn-1 (in bounds); the softmax masks those keys.
+template <int NW>
+__device__ __forceinline__ void issue_tile(char* stage, const uint16_t* kbase,
                                            const uint16_t* vbase, size_t stride, int tn) {
-  // 64 rows x 256 bytes = 1024 16-byte pieces per tensor
+  constexpr int kLoads = 32 / NW;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wid = threadIdx.x / kWave;
 #pragma unroll
-  for (int it = 0; it < 1024 / NT; ++it) {
-    const int piece = it * NT + threadIdx.x;
-    const int row = piece >> 4;
-    const int col = (piece & 15) * 8;
-    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-    if (row < tn) {
-      kv = *reinterpret_cast<const uint4*>(kbase + size_t(row) * stride + col);
-      vv = *reinterpret_cast<const uint4*>(vbase + size_t(row) * stride + col);
-    }
-    *reinterpret_cast<uint4*>(s_k + row * kRowHalfs + col) = kv;
-    *reinterpret_cast<uint4*>(s_v + row * kRowHalfs + col) = vv;
+  for (int j = 0; j < kLoads; ++j) {
+    const int q = wid * kLoads + j;  // 0..31, uniform in the wave
+    const int tensor = q >> 4;
+    const int rg = q & 15;
+    const int row = rg * 4 + (lane >> 4);
+    const int c = (lane & 15) ^ (row & 15);
+    const int srow = row < tn ? row : tn - 1;
+    const uint16_t* src = (tensor ? vbase : kbase) + size_t(srow) * stride + c * 8;
+    __builtin_amdgcn_global_load_lds(src, (lds_void_t*)(stage + tensor * kTileBytes + rg * 1024),
+                                     16, 0, 0);
   }
 }
 
-struct TileState {
-  floatx4 o[8];   // O^T: lane holds dims 16*dt + 4*(lane/16) + i of row lane%16
-  float m;        // running max, log2 units
-  float l;        // this lane's share of the running sum
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  // gfx9 s_waitcnt encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]
+  constexpr int imm = (N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14);
+  __builtin_amdgcn_s_waitcnt(imm);
+}
+
+struct RowTile {
+  floatx4 o[8];  // O^T: lane holds dims 16*dt + 4*(lane/16) + i of row lane%16
+  float m;       // running max of scaled logits (log2 units)
+  float l;       // this lane's share of the running sum
 };
 
-// One 64-key LDS tile against the wave's row tiles.
-// valid_keys: keys [0, valid_keys) of the tile exist.  mask_word(t, h): for the
-// tree tail, the 32-bit visibility word of this lane's row for keys [32h, 32h+32)
-// of the tile (all ones for the prefix).
-template <int MT, bool kTail>
-__device__ __forceinline__ void process_tile(const uint16_t* s_k, const uint16_t* s_v,
-                                             const bf16x8 (*qf)[4], TileState* ts, int ntiles,
-                                             int valid_keys, float scale2,
-                                             const uint32_t (*mword)[2]) {
+// Per-lane LDS byte offsets of the swizzled fragment reads (lane constants; the
+// subtile / key-block parts are compile-time immediates on top of these).
+struct LaneOffsets {
+  int k[4];  // K A-fragment of chunk 4*kk + lg, row lr of a 16-key subtile
+  int v[8];  // V^T transposed read of dims 16*dt + 4*(lr&3), key 4*lg + (lr>>2) of a 16-key block
+};
+
+__device__ __forceinline__ LaneOffsets lane_offsets() {
   const int lane = threadIdx.x & (kWave - 1);
-  const int lr = lane & 15;  // row within a tile (S^T column) / key within a subtile (A row)
-  const int lg = lane >> 4;  // k-group
-#pragma unroll 1
-  for (int h = 0; h < 2; ++h) {
-    // K fragments of the two 16-key subtiles of this 32-key block
-    bf16x8 kf[2][4];
+  const int lr = lane & 15, lg = lane >> 4;
+  LaneOffsets o;
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      const uint16_t* krow = s_k + (32 * h + 16 * st + lr) * kRowHalfs;
+  for (int kk = 0; kk < 4; ++kk) o.k[kk] = swz(lr, 4 * kk + lg);
+  const int key = 4 * lg + (lr >> 2);
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        kf[st][kk] = as_bf16x8(*reinterpret_cast<const uint4*>(krow + 32 * kk + 8 * lg));
-    }
-    bf16x8 pf[MT];
+  for (int dt = 0; dt < 8; ++dt) {
+    const int d = 16 * dt + 4 * (lr & 3);
+    o.v[dt] = swz(key, d >> 3) + ((d & 4) << 1);
+  }
+  return o;
+}
+
+// One 64-key tile from LDS against the wave's row tiles.
+// masked: keys >= tn are invisible, and key j is visible to a row only if bit j
+// (of this tile's 64) is set in its mask words.
+template <int MT>
+__device__ __forceinline__ void compute_tile(const char* kt, const char* vt, const bf16x8 (*qf)[4],
+                                             RowTile* rt, int ntiles, bool masked, int tn,
+                                             float scale2, const uint32_t (*mword)[2],
+                                             const LaneOffsets& lo) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int lg = lane >> 4;
+  // S^T = K Q^T for the 4 subtiles of 16 keys (subtile s4 = rows 16*s4.., +4096 bytes)
+  floatx4 st[MT][4];
+#pragma unroll
+  for (int s4 = 0; s4 < 4; ++s4) {
+    bf16x8 kf[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+      kf[kk] = *reinterpret_cast<const bf16x8*>(kt + lo.k[kk] + 4096 * s4);
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
       if (t >= ntiles) break;
-      floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[0][kk], qf[t][kk], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[1][kk], qf[t][kk], s1, 0, 0, 0);
-      }
-      // lane holds keys 32h + 4lg + i (s0) and 32h + 16 + 4lg + i (s1) of row lr
-      float sv[8];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int k0 = 32 * h + 4 * lg + i;
-        const int k1 = k0 + 16;
-        bool v0 = k0 < valid_keys, v1 = k1 < valid_keys;
-        if (kTail) {
-          v0 = v0 && ((mword[t][h] >> (4 * lg + i)) & 1u);
-          v1 = v1 && ((mword[t][h] >> (16 + 4 * lg + i)) & 1u);
-        }
-        sv[i] = v0 ? s0[i] * scale2 : -__builtin_inff();
-        sv[4 + i] = v1 ? s1[i] * scale2 : -__builtin_inff();
-      }
-      float mx = sv[0];
-#pragma unroll
-      for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-      const float m_new = fmaxf(ts[t].m, mx);
-      const float m_use = m_new == -__builtin_inff() ? 0.0f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(ts[t].m - m_use);
-      float psum = 0.0f;
-      float p[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        p[e] = __builtin_amdgcn_exp2f(sv[e] - m_use);
-        psum += p[e];
-      }
-      ts[t].l = ts[t].l * alpha + psum;
-      ts[t].m = m_new;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) ts[t].o[dt] *= alpha;
-      uint4 pk;
-      pk.x = pack_bf16x2(p[0], p[1]);
-      pk.y = pack_bf16x2(p[2], p[3]);
-      pk.z = pack_bf16x2(p[4], p[5]);
-      pk.w = pack_bf16x2(p[6], p[7]);
-      pf[t] = as_bf16x8(pk);
+      for (int kk = 0; kk < 4; ++kk)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kk], qf[t][kk], acc, 0, 0, 0);
+      st[t][s4] = acc;
     }
-    // O^T += V^T P^T; V^T fragment: dim 16dt + lr, keys 32h + {4lg..4lg+3, 16+4lg..16+4lg+3}
+  }
+  // online softmax (base 2); lane holds keys 16*s4 + 4*lg + i of row lane%16
+  bf16x8 pf[MT][2];
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      const uint16_t* vcol = s_v + 16 * dt + lr;
-      uint16_t e[8];
+  for (int t = 0; t < MT; ++t) {
+    if (t >= ntiles) break;
+    float sv[16];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        e[i] = vcol[(32 * h + 4 * lg + i) * kRowHalfs];
-        e[4 + i] = vcol[(32 * h + 16 + 4 * lg + i) * kRowHalfs];
-      }
-      uint4 vv;
-      vv.x = uint32_t(e[0]) | (uint32_t(e[1]) << 16);
-      vv.y = uint32_t(e[2]) | (uint32_t(e[3]) << 16);
-      vv.z = uint32_t(e[4]) | (uint32_t(e[5]) << 16);
-      vv.w = uint32_t(e[6]) | (uint32_t(e[7]) << 16);
-      const bf16x8 vf = as_bf16x8(vv);
+    for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sv[4 * s4 + i] = st[t][s4][i];
+    if (masked) {
+      // key >> 5 == s4 >> 1 because 4 * lg + i < 16
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = 16 * s4 + 4 * lg + i;
+          const bool ok = key < tn && ((mword[t][s4 >> 1] >> (key & 31)) & 1u);
+          sv[4 * s4 + i] = ok ? sv[4 * s4 + i] : -__builtin_inff();
+        }
+    }
+    float mx = sv[0];
+#pragma unroll
+    for (int e = 1; e < 16; ++e) mx = fmaxf(mx, sv[e]);
+    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    const float mt = mx * scale2;  // -inf stays -inf
+    const float m_new = fmaxf(rt[t].m, mt);
+    if (__ballot(m_new > rt[t].m) != 0ull) {
+      const float alpha = __builtin_amdgcn_exp2f(rt[t].m - m_new);  // 0 for -inf, 1 if unchanged
+      rt[t].l *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) rt[t].o[dt] *= alpha;
+      rt[t].m = m_new;
+    }
+    const float neg_m = m_new == -__builtin_inff() ? 0.0f : -m_new;
+    float psum = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      sv[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[e], scale2, neg_m));
+      psum += sv[e];
+    }
+    rt[t].l += psum;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      uint4 pk;
+      pk.x = pack_bf16x2(sv[8 * h + 0], sv[8 * h + 1]);
+      pk.y = pack_bf16x2(sv[8 * h + 2], sv[8 * h + 3]);
+      pk.z = pack_bf16x2(sv[8 * h + 4], sv[8 * h + 5]);
+      pk.w = pack_bf16x2(sv[8 * h + 6], sv[8 * h + 7]);
+      pf[t][h] = as_bf16x8(pk);
+    }
+  }
+  // O^T += V^T P^T.  V^T fragment via transposed LDS reads: input lane i of block lg
+  // reads 4 dims of one key, output lane j gets dim j of 4 keys.
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      char* base = const_cast<char*>(vt) + lo.v[dt] + 8192 * h;  // keys 32h.. (+16 keys = 4096 B)
+      const shortx4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(base));
+      const shortx4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(base + 4096));
+      const bf16x8 vf =
+          __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
       for (int t = 0; t < MT; ++t) {
         if (t >= ntiles) break;
-        ts[t].o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[t], ts[t].o[dt], 0, 0, 0);
+        rt[t].o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[t][h], rt[t].o[dt], 0, 0, 0);
       }
     }
   }
 }
 
-template <int NW, int MT>
+template <int NW, int MT, int STAGES>
 __global__ __launch_bounds__(NW * kWave) void attn_main_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_new,
     const uint16_t* __restrict__ v_new, const uint16_t* __restrict__ k_cache,
     const uint16_t* __restrict__ v_cache, const uint32_t* __restrict__ tree_mask, int W, int hq,
     int hkv, int G, float scale2, AttnWs ws) {
-  __shared__ __attribute__((aligned(16))) uint16_t s_k[kTileKeys * kRowHalfs];
-  __shared__ __attribute__((aligned(16))) uint16_t s_v[kTileKeys * kRowHalfs];
+  __shared__ __attribute__((aligned(1024))) char s_ring[STAGES * kStageBytes];
+  constexpr int kLoads = 32 / NW;
+  constexpr int kRowsPerPass = NW * MT * 16;
 
   const int n_items = ws.meta[0];
-  const int item_id = blockIdx.x;
-  if (item_id >= n_items) return;
-  const Item it = ws.items[item_id];
+  if (int(blockIdx.x) >= n_items) return;
+  const Item it = ws.items[blockIdx.x];
   const PairInfo pi = ws.pairs[it.pair];
   const int kvh = it.pair % hkv;
   const bool last = (it.part >> 30) & 1;
   const int part = it.part & ((1 << 30) - 1);
   const int rows = pi.nslots * G;
-  constexpr int NT = NW * kWave;
-  constexpr int kRowsPerPass = NW * MT * 16;
   const int lane = threadIdx.x & (kWave - 1);
   const int wid = threadIdx.x / kWave;
   const int lr = lane & 15, lg = lane >> 4;
-  const size_t kv_stride = size_t(hkv) * kD;
+  const size_t stride = size_t(hkv) * kD;
+  const int ntk = (it.ke - it.kb + kTileKeys - 1) / kTileKeys;
+  const uint16_t* kpre = k_cache + size_t(it.kb) * stride + kvh * kD;
+  const uint16_t* vpre = v_cache + size_t(it.kb) * stride + kvh * kD;
+  const LaneOffsets lo = lane_offsets();
 
   for (int pass = 0; pass * kRowsPerPass < rows; ++pass) {
-    // row tiles of this wave: pass * NW * MT + wid + NW * t
     int ntiles = 0;
     bf16x8 qf[MT][4];
-    TileState ts[MT];
-    uint32_t mword[MT][2];
-    int row_of_lane[MT];
+    RowTile rt[MT];
+    int rho_t[MT];
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
       const int tile = pass * NW * MT + wid + NW * t;
       const int rho = tile * 16 + lr;
-      row_of_lane[t] = rho;
+      rho_t[t] = rho;
       if (tile * 16 < rows) ntiles = t + 1;
-      uint4 z = make_uint4(0, 0, 0, 0);
-      uint4 qv[4] = {z, z, z, z};
+      uint4 qv[4] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0),
+                     make_uint4(0, 0, 0, 0)};
       if (rho < rows) {
-        const int slot = pi.q0 + rho / G;
-        const int head = kvh * G + rho % G;
-        const uint16_t* qrow = q + (size_t(slot) * hq + head) * kD;
+        const uint16_t* qrow = q + (size_t(pi.q0 + rho / G) * hq + kvh * G + rho % G) * kD;
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk)
           qv[kk] = *reinterpret_cast<const uint4*>(qrow + 32 * kk + 8 * lg);
@@ -353,59 +414,84 @@ __global__ __launch_bounds__(NW * kWave) void attn_main_kernel(
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) qf[t][kk] = as_bf16x8(qv[kk]);
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) ts[t].o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-      ts[t].m = -__builtin_inff();
-      ts[t].l = 0.0f;
+      for (int dt = 0; dt < 8; ++dt) rt[t].o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      rt[t].m = -__builtin_inff();
+      rt[t].l = 0.0f;
     }
+    wait_vm<0>();  // Q (and earlier stores) done: vmcnt now counts tile copies only
 
-    // prefix chunk
-    for (int t0 = it.kb; t0 < it.ke; t0 += kTileKeys) {
-      const int tn = min(kTileKeys, it.ke - t0);
-      stage_tile<NT>(s_k, s_v, k_cache + size_t(t0) * kv_stride + kvh * kD,
-                     v_cache + size_t(t0) * kv_stride + kvh * kD, kv_stride, tn);
-      __syncthreads();
-      if (ntiles > 0) process_tile<MT, false>(s_k, s_v, qf, ts, ntiles, tn, scale2, nullptr);
-      __syncthreads();
-    }
-    // tree tail: the request's own slots, visible through the ancestor bitmask
-    if (last) {
-      for (int j0 = 0; j0 < pi.nslots; j0 += kTileKeys) {
-        const int tn = min(kTileKeys, pi.nslots - j0);
-        stage_tile<NT>(s_k, s_v, k_new + size_t(pi.q0 + j0) * kv_stride + kvh * kD,
-                       v_new + size_t(pi.q0 + j0) * kv_stride + kvh * kD, kv_stride, tn);
+    // The item's tiles: the prefix chunk through a STAGES-deep ring of LDS tiles,
+    // then (last chunk only) the tree tail, one synchronous tile at a time.
+    const int ntail = last ? (pi.nslots + kTileKeys - 1) / kTileKeys : 0;
+    uint32_t mword[MT][2];
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+      if (s < ntk)
+        issue_tile<NW>(s_ring + s * kStageBytes, kpre + size_t(s) * kTileKeys * stride,
+                       vpre + size_t(s) * kTileKeys * stride, stride,
+                       min(kTileKeys, it.ke - it.kb - s * kTileKeys));
+    for (int i = 0; i < ntk + ntail; ++i) {
+      const char* stg;
+      int tn;
+      if (i < ntk) {
+        const int ahead = min(STAGES - 2, ntk - 1 - i);  // tiles issued after tile i
+        if (ahead >= 2) wait_vm<2 * kLoads>();
+        else if (ahead == 1) wait_vm<kLoads>();
+        else wait_vm<0>();
+        __syncthreads();
+        const int nx = i + STAGES - 1;
+        if (nx < ntk)
+          issue_tile<NW>(s_ring + (nx % STAGES) * kStageBytes,
+                         kpre + size_t(nx) * kTileKeys * stride,
+                         vpre + size_t(nx) * kTileKeys * stride, stride,
+                         min(kTileKeys, it.ke - it.kb - nx * kTileKeys));
+        stg = s_ring + (i % STAGES) * kStageBytes;
+        tn = min(kTileKeys, it.ke - it.kb - i * kTileKeys);
+#pragma unroll
+        for (int t = 0; t < MT; ++t) mword[t][0] = mword[t][1] = 0xFFFFFFFFu;
+      } else {
+        // tree tail: the request's own slots, visible through the ancestor bitmask
+        const int j0 = (i - ntk) * kTileKeys;
+        tn = min(kTileKeys, pi.nslots - j0);
+        __syncthreads();  // every wave is done with the previous tile's stage
+        issue_tile<NW>(s_ring, k_new + size_t(pi.q0 + j0) * stride + kvh * kD,
+                       v_new + size_t(pi.q0 + j0) * stride + kvh * kD, stride, tn);
 #pragma unroll
         for (int t = 0; t < MT; ++t) {
           mword[t][0] = 0u;
           mword[t][1] = 0u;
-          const int rho = row_of_lane[t];
-          if (rho < rows) {
-            const uint32_t* mrow = tree_mask + size_t(pi.q0 + rho / G) * W;
+          if (rho_t[t] < rows) {
+            const uint32_t* mrow = tree_mask + size_t(pi.q0 + rho_t[t] / G) * W;
             const int w0 = j0 >> 5;
             if (w0 < W) mword[t][0] = mrow[w0];
             if (w0 + 1 < W) mword[t][1] = mrow[w0 + 1];
           }
         }
+        wait_vm<0>();
         __syncthreads();
-        if (ntiles > 0) process_tile<MT, true>(s_k, s_v, qf, ts, ntiles, tn, scale2, mword);
-        __syncthreads();
+        stg = s_ring;
       }
+      if (ntiles > 0)
+        compute_tile<MT>(stg, stg + kTileBytes, qf, rt, ntiles, tn < kTileKeys || i >= ntk, tn,
+                         scale2, mword, lo);
     }
-    // partial results
+    __syncthreads();
+    // partial results of this chunk
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
       if (t >= ntiles) break;
-      float l = ts[t].l;
+      float l = rt[t].l;
       l += __shfl_xor(l, 16, kWave);
       l += __shfl_xor(l, 32, kWave);
-      const int rho = row_of_lane[t];
+      const int rho = rho_t[t];
       if (rho < rows) {
         const size_t prow = size_t(pi.part_base) + size_t(part) * rows + rho;
         float* po = ws.part_o + prow * kD;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt)
-          *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = ts[t].o[dt];
+          *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = rt[t].o[dt];
         if (lg == 0) {
-          ws.part_ml[prow * 2 + 0] = ts[t].m;
+          ws.part_ml[prow * 2 + 0] = rt[t].m;
           ws.part_ml[prow * 2 + 1] = l;
         }
       }
@@ -414,46 +500,53 @@ __global__ __launch_bounds__(NW * kWave) void attn_main_kernel(
 }
 
 // ------------------------------------------------------------- combine ----
+// One workgroup per group of 8 rows of one pair; thread = (row, 4 dims).  All
+// chunk partials of a row are loaded independently, then merged in chunk order.
 __global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv, int G, AttnWs ws,
                                                                 float* __restrict__ out,
                                                                 float* __restrict__ lse) {
-  const int pr = blockIdx.x;
-  const PairInfo pi = ws.pairs[pr];
-  if (pi.nparts == 0) return;
-  const int kvh = pr % hkv;
+  if (int(blockIdx.x) >= ws.meta[1]) return;
+  const int2 cg = ws.cgroups[blockIdx.x];
+  const PairInfo pi = ws.pairs[cg.x];
+  const int kvh = cg.x % hkv;
   const int rows = pi.nslots * G;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int wid = threadIdx.x / kWave;
-  for (int rho = wid; rho < rows; rho += kWaves) {
-    float M = -__builtin_inff();
-    for (int i = 0; i < pi.nparts; ++i) {
+  const int rho = cg.y + (threadIdx.x >> 5);
+  const int d4 = (threadIdx.x & 31) * 4;
+  if (rho >= rows) return;
+  float mv[kMaxParts], lv[kMaxParts];
+  float M = -__builtin_inff();
+#pragma unroll
+  for (int i = 0; i < kMaxParts; ++i) {
+    mv[i] = -__builtin_inff();
+    lv[i] = 0.0f;
+    if (i < pi.nparts) {
       const size_t prow = size_t(pi.part_base) + size_t(i) * rows + rho;
-      M = fmaxf(M, ws.part_ml[prow * 2]);
+      const float2 ml = *reinterpret_cast<const float2*>(ws.part_ml + prow * 2);
+      mv[i] = ml.x;
+      lv[i] = ml.y;
+      M = fmaxf(M, ml.x);
     }
-    const float Mu = M == -__builtin_inff() ? 0.0f : M;
-    float L = 0.0f, o0 = 0.0f, o1 = 0.0f;
-    for (int i = 0; i < pi.nparts; ++i) {
-      const size_t prow = size_t(pi.part_base) + size_t(i) * rows + rho;
-      const float w = __builtin_amdgcn_exp2f(ws.part_ml[prow * 2] - Mu);
-      L += w * ws.part_ml[prow * 2 + 1];
-      const float2 v = *reinterpret_cast<const float2*>(ws.part_o + prow * kD + 2 * lane);
-      o0 += w * v.x;
-      o1 += w * v.y;
-    }
-    const int slot = pi.q0 + rho / G;
-    const int head = kvh * G + rho % G;
-    float* orow = out + (size_t(slot) * hq + head) * kD;
-    float2 res;
-    if (L > 0.0f) {
-      const float inv = 1.0f / L;
-      res = make_float2(o0 * inv, o1 * inv);
-    } else {
-      res = make_float2(0.0f, 0.0f);
-    }
-    *reinterpret_cast<float2*>(orow + 2 * lane) = res;
-    if (lse != nullptr && lane == 0)
-      lse[size_t(slot) * hq + head] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
   }
+  const float Mu = M == -__builtin_inff() ? 0.0f : M;
+  float L = 0.0f;
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < kMaxParts; ++i) {
+    if (i < pi.nparts) {
+      const size_t prow = size_t(pi.part_base) + size_t(i) * rows + rho;
+      const float w = __builtin_amdgcn_exp2f(mv[i] - Mu);
+      L += w * lv[i];
+      const floatx4 v = *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
+      acc += w * v;
+    }
+  }
+  const int slot = pi.q0 + rho / G;
+  const int head = kvh * G + rho % G;
+  float* orow = out + (size_t(slot) * hq + head) * kD + d4;
+  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+  *reinterpret_cast<floatx4*>(orow) = acc * inv;
+  if (lse != nullptr && d4 == 0)
+    lse[size_t(slot) * hq + head] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
 }
 
 int target_items_for_device() { return 8 * device_cu_count(); }
@@ -462,30 +555,31 @@ int target_items_for_device() { return 8 * device_cu_count(); }
 
 size_t attn_workspace_bytes(int32_t R, int32_t max_rows, int32_t hq, int32_t hkv) {
   const size_t icap = item_capacity(R, hkv, target_items_for_device());
+  const size_t cgcap = cgroup_capacity(R, max_rows, hq, hkv);
   const size_t part_rows = size_t(kMaxParts) * max_rows * hq;
   return 256 + al(icap * sizeof(Item)) + al(size_t(R) * hkv * sizeof(PairInfo)) +
-         al(part_rows * 2 * sizeof(float)) + al(part_rows * kD * sizeof(float));
+         al(cgcap * sizeof(int2)) + al(part_rows * 2 * sizeof(float)) +
+         al(part_rows * kD * sizeof(float));
 }
 
 int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
   const int target = target_items_for_device();
   const size_t icap = item_capacity(a.R, a.hkv, target);
+  const size_t cgcap = cgroup_capacity(a.R, a.max_rows, a.hq, a.hkv);
   const size_t part_rows = size_t(kMaxParts) * a.max_rows * a.hq;
-  AttnWs ws = attn_layout(a.workspace, a.R, a.hkv, icap, part_rows);
+  AttnWs ws = attn_layout(a.workspace, a.R, a.hkv, icap, cgcap, part_rows);
   const int G = a.hq / a.hkv;
-  if (a.R == 0) return ECHO_OK;
   hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kThreads), 0, stream, a.q_offsets,
                      a.kv_offsets, static_cast<long long>(a.kv_rows), a.R, a.hkv, G, a.max_rows,
                      target, ws, a.status);
   const bool prof = g_attn_ev_start != nullptr && g_attn_ev_stop != nullptr;
   if (prof && hipEventRecord(g_attn_ev_start, stream) != hipSuccess) return ECHO_ERR_HIP;
-  hipLaunchKernelGGL((attn_main_kernel<kMainWaves, kMT>), dim3(unsigned(icap)),
-                     dim3(kMainWaves * kWave), 0, stream, a.q,
-                     a.k_new, a.v_new, a.k_cache, a.v_cache, a.tree_mask, a.mask_words, a.hq,
-                     a.hkv, G, a.sm_scale * kLog2e, ws);
+  hipLaunchKernelGGL((attn_main_kernel<kMainWaves, kMT, kStages>), dim3(unsigned(icap)),
+                     dim3(kMainWaves * kWave), 0, stream, a.q, a.k_new, a.v_new, a.k_cache,
+                     a.v_cache, a.tree_mask, a.mask_words, a.hq, a.hkv, G, a.sm_scale * kLog2e, ws);
   if (prof && hipEventRecord(g_attn_ev_stop, stream) != hipSuccess) return ECHO_ERR_HIP;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(a.R * a.hkv)), dim3(kThreads), 0, stream,
-                     a.hq, a.hkv, G, ws, a.out, a.lse);
+  hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(cgcap)), dim3(kCombineRows * 32), 0,
+                     stream, a.hq, a.hkv, G, ws, a.out, a.lse);
   return hipGetLastError() == hipSuccess ? ECHO_OK : ECHO_ERR_HIP;
 }
 
