@@ -73,6 +73,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise EchoError(f"{path} is missing: build it with "
                         "`python -m paper_2604_09603_amd.build` (there is no CPU fallback)")
+    # torch ships its own HIP runtime under the same soname; load it first so that the
+    # library and torch's streams and allocations share one runtime instance
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     for name, (res, args) in _SIGS.items():
         fn = getattr(lib, name)

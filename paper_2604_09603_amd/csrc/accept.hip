@@ -80,6 +80,7 @@ int32_t launch_accept(const int32_t* q_offsets, const int32_t* slot_parent,
                       int32_t max_rows, int32_t max_depth, int32_t* accept_len,
                       int32_t* accept_slots, int32_t* bonus_token, int32_t* status,
                       hipStream_t stream) {
+  (void)hipGetLastError();  // clear errors left by unrelated runtime calls
   if (R == 0) return ECHO_OK;
   hipLaunchKernelGGL(accept_kernel, dim3(R), dim3(kWave), 0, stream, q_offsets, slot_parent,
                      slot_token, target_token, max_rows, max_depth, accept_len, accept_slots,

@@ -1,21 +1,23 @@
 // Tree-masked grouped-query verification attention (one verification forward
 // over the flattened super-tree).  Three launches:
 //
-//   attn_plan     one workgroup: per (request, kv head) pair, split the KV
-//                 prefix into chunks so that the whole batch yields about
-//                 `target_items` work items; write the item list and each
-//                 pair's slice of the partial-result buffer.
-//   attn_main     one workgroup (4 waves) per item.  The item's KV chunk is
-//                 streamed HBM -> LDS once, 64 keys at a time, and shared by
-//                 every row of the pair: rows are (slot, query head in the
-//                 GQA group), slot-major, in 16-row MFMA tiles spread over
-//                 the waves.  S^T = K Q^T and O^T = V^T P^T on
-//                 v_mfma_f32_16x16x32_bf16 with fp32 accumulation; online
-//                 softmax in base 2.  The last chunk of a pair also runs the
-//                 tree tail: the new keys of the request's own slots, masked
-//                 by the ancestor bitmask.  Output: unnormalised partial O,
-//                 running max and sum per row.
-//   attn_combine  one workgroup per pair: merge the chunk partials in chunk
+//   attn_plan     one workgroup.  The work is a stream of 32-key tiles: for each
+//                 (request, kv head) pair and each 128-row pass over its rows
+//                 (rows = verify slots x query heads of the GQA group), first
+//                 the tree-tail tiles (the new keys of the request's own slots)
+//                 and then the KV-prefix tiles.  The stream is cut into equal
+//                 contiguous ranges, one per workgroup of the main kernel; the
+//                 plan records each unit's tiles and which units are cut.
+//   attn_main     persistent, two workgroups (4 waves each) per CU.  Each
+//                 workgroup streams its range HBM -> LDS through a 4-stage
+//                 ring of direct-to-LDS copies that runs across unit
+//                 boundaries; every tile is shared by all rows of its unit.
+//                 S^T = K Q^T and O^T = V^T P^T on v_mfma_f32_16x16x32_bf16
+//                 (fp32 accumulation), online softmax in base 2, ancestor
+//                 bitmask on tree-tail tiles.  A unit that lies inside one
+//                 range is normalised and written to out/lse directly; a cut
+//                 unit leaves one partial (O, max, sum) per workgroup.
+//   attn_combine  one workgroup per cut unit: merges its partials in range
 //                 order (deterministic) into out and lse.
 #include "echo_device.h"
 #include "echo_internal.h"
@@ -25,172 +27,191 @@ namespace {
 
 constexpr int kD = ECHO_HEAD_DIM;   // 128
 constexpr int kThreads = 256;       // plan / combine workgroups
-constexpr int kWaves = kThreads / kWave;
-constexpr int kMainWaves = 8;       // main kernel: waves per workgroup
-constexpr int kMT = 2;              // 16-row tiles per wave per row pass
-constexpr int kStages = 4;          // LDS ring depth (64-key K+V tiles)
-constexpr int kCombineRows = 8;     // rows per combine workgroup
-constexpr int kTileKeys = 64;       // keys staged in LDS per step
-constexpr int kMaxParts = 16;       // chunks per pair at most
-constexpr int kChunkMin = 256;      // shortest chunk (keys)
+constexpr int kMainWaves = 4;       // main kernel: waves per workgroup (two workgroups per CU)
+constexpr int kMT = 2;              // 16-row tiles per wave
+constexpr int kPassRows = kMainWaves * kMT * 16;  // rows per unit (128)
+constexpr int kStages = 4;          // LDS ring depth (32-key K+V tiles, 16 KB each)
+constexpr int kTileKeys = 32;       // keys per tile
+constexpr int kMaskWords = 4;       // tree-tail mask words preloaded per unit (128 slots)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-struct Item {
-  int32_t pair;    // r * Hkv + kvh
-  int32_t kb, ke;  // prefix rows [kb, ke) of the KV cache (token index)
-  int32_t part;    // chunk index within the pair; bit 30 set: last chunk (runs the tree tail)
+// One unit of the tile stream: a row pass of one (request, kv head) pair.
+struct Unit {
+  int32_t tile_start, tile_end;  // global tile range: ntail tail tiles, then prefix tiles
+  int32_t q0, nslots;            // the request's verify slots
+  int32_t row0, rows;            // rows [row0, row0 + rows) of the pair (slot-major, G per slot)
+  int32_t kb, P;                 // KV prefix rows [kb, kb + P)
+  int32_t kvh, ntail;            // kv head; ceil(nslots / 32)
+  int32_t cut, pad;              // cut: covered by more than one workgroup
 };
 
-struct PairInfo {
-  int32_t part_base;  // first partial row of this pair
-  int32_t nparts;     // 0: request skipped
-  int32_t q0;         // first slot of the request
-  int32_t nslots;
+struct Cut {
+  int32_t unit, b0, b1, first_slot;  // workgroups b0..b1; partial slot of b0's segment
 };
 
 struct AttnWs {
-  int32_t* meta;     // [0] = number of items, [1] = number of combine groups
-  Item* items;
-  PairInfo* pairs;
-  int2* cgroups;     // (pair, first row) of each combine workgroup
-  float* part_ml;    // [rows][2]: running max (log2 units), sum
-  float* part_o;     // [rows][128]
+  int32_t* meta;   // [0] = units, [1] = tiles, [2] = cut units
+  Unit* units;
+  int32_t* wg_unit;  // [nb] unit holding each workgroup's first tile
+  Cut* cuts;
+  float* part_ml;  // [2 * nb * 128][2]: running max (log2 units), sum
+  float* part_o;   // [2 * nb * 128][128]
 };
 
 __host__ __device__ inline size_t al(size_t x) { return (x + 255) / 256 * 256; }
 
-__host__ inline size_t item_capacity(int R, int hkv, int target_items) {
-  return size_t(target_items) + size_t(R) * hkv;
+__host__ inline size_t unit_capacity(int R, int max_rows, int hq, int hkv) {
+  return size_t(R) * hkv + (size_t(max_rows) * hq + kPassRows - 1) / kPassRows;
 }
 
-__host__ inline size_t cgroup_capacity(int R, int max_rows, int hq, int hkv) {
-  return (size_t(max_rows) * hq + kCombineRows - 1) / kCombineRows + size_t(R) * hkv;
-}
-
-__host__ __device__ inline AttnWs attn_layout(void* base, int R, int hkv, size_t item_cap,
-                                              size_t cg_cap, size_t part_rows) {
+__host__ __device__ inline AttnWs attn_layout(void* base, size_t ucap, int nb) {
   char* p = static_cast<char*>(base);
   AttnWs w;
   w.meta = reinterpret_cast<int32_t*>(p);
   p += 256;
-  w.items = reinterpret_cast<Item*>(p);
-  p += al(item_cap * sizeof(Item));
-  w.pairs = reinterpret_cast<PairInfo*>(p);
-  p += al(size_t(R) * hkv * sizeof(PairInfo));
-  w.cgroups = reinterpret_cast<int2*>(p);
-  p += al(cg_cap * sizeof(int2));
+  w.units = reinterpret_cast<Unit*>(p);
+  p += al(ucap * sizeof(Unit));
+  w.wg_unit = reinterpret_cast<int32_t*>(p);
+  p += al(size_t(nb) * sizeof(int32_t));
+  w.cuts = reinterpret_cast<Cut*>(p);
+  p += al(size_t(nb) * sizeof(Cut));
   w.part_ml = reinterpret_cast<float*>(p);
-  p += al(part_rows * 2 * sizeof(float));
+  p += al(size_t(2) * nb * kPassRows * 2 * sizeof(float));
   w.part_o = reinterpret_cast<float*>(p);
   return w;
 }
 
+__host__ inline size_t attn_ws_total(size_t ucap, int nb) {
+  return 256 + al(ucap * sizeof(Unit)) + al(size_t(nb) * 4) + al(size_t(nb) * sizeof(Cut)) +
+         al(size_t(2) * nb * kPassRows * 2 * 4) + al(size_t(2) * nb * kPassRows * kD * 4);
+}
+
+// First tile of workgroup b when T tiles are cut into nb equal ranges.
+__device__ __forceinline__ long long range_lo(long long T, int b, int nb) { return T * b / nb; }
+// Workgroup whose range holds tile t.
+__device__ __forceinline__ int range_of(long long t, long long T, int nb) {
+  return int(((t + 1) * nb + T - 1) / T) - 1;
+}
+
 // ---------------------------------------------------------------- plan ----
+__device__ __forceinline__ bool pair_ok(const int32_t* q_offsets, const int64_t* kv_offsets,
+                                        long long kv_rows, int max_rows, int r) {
+  const int q0 = q_offsets[r], q1 = q_offsets[r + 1];
+  const long long k0 = kv_offsets[r], k1 = kv_offsets[r + 1];
+  return q0 >= 0 && q1 >= q0 && q1 <= max_rows && k0 >= 0 && k1 >= k0 && k1 <= kv_rows;
+}
+
 __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
     const int32_t* __restrict__ q_offsets, const int64_t* __restrict__ kv_offsets,
-    long long kv_rows, int R, int hkv, int G, int max_rows, int target_items, AttnWs ws,
-    int32_t* status) {
+    long long kv_rows, int R, int hkv, int G, int max_rows, int nb, AttnWs ws, int32_t* status) {
   __shared__ int s_scan[kThreads / kWave + 1];
-  __shared__ long long s_total;
   const int tid = threadIdx.x;
-  // total prefix keys over valid requests
-  long long my = 0;
-  int bits = 0;
-  for (int r = tid; r < R; r += kThreads) {
-    const int q0 = q_offsets[r], q1 = q_offsets[r + 1];
-    const long long k0 = kv_offsets[r], k1 = kv_offsets[r + 1];
-    const bool ok = q0 >= 0 && q1 >= q0 && q1 <= max_rows && k0 >= 0 && k1 >= k0 && k1 <= kv_rows;
-    if (!ok) bits |= ECHO_DATA_BAD_OFFSETS;
-    else if (q1 > q0) my += k1 - k0;
-  }
-  wave_status_or(status, bits);
-  if (tid == 0) s_total = 0;
-  __syncthreads();
-  atomicAdd(reinterpret_cast<unsigned long long*>(&s_total), static_cast<unsigned long long>(my));
-  __syncthreads();
-  const long long total = s_total * hkv;
-  long long ch = (total + target_items - 1) / target_items;
-  ch = (ch + kTileKeys - 1) / kTileKeys * kTileKeys;
-  if (ch < kChunkMin) ch = kChunkMin;
-
-  // pairs in request-major order; scan their item counts, partial rows, combine groups
-  int item_run = 0, row_run = 0, cg_run = 0;
   const int npairs = R * hkv;
+  int bits = 0;
+  for (int r = tid; r < R; r += kThreads)
+    if (!pair_ok(q_offsets, kv_offsets, kv_rows, max_rows, r)) bits |= ECHO_DATA_BAD_OFFSETS;
+  wave_status_or(status, bits);
+
+  // pass A: total tiles
+  long long T = 0;
   for (int base = 0; base < npairs; base += kThreads) {
     const int pr = base + tid;
-    int nparts = 0, rows = 0, q0 = 0, nsl = 0;
-    long long k0 = 0, len = 0, chr = ch;
+    int tiles = 0;
     if (pr < npairs) {
       const int r = pr / hkv;
-      q0 = q_offsets[r];
-      const int q1 = q_offsets[r + 1];
-      k0 = kv_offsets[r];
-      const long long k1 = kv_offsets[r + 1];
-      const bool ok =
-          q0 >= 0 && q1 >= q0 && q1 <= max_rows && k0 >= 0 && k1 >= k0 && k1 <= kv_rows;
-      if (ok && q1 > q0) {
-        nsl = q1 - q0;
-        rows = nsl * G;
-        len = k1 - k0;
-        long long np = (len + ch - 1) / ch;
-        if (np < 1) np = 1;
-        if (np > kMaxParts) {
-          np = kMaxParts;
-          chr = (len + kMaxParts - 1) / kMaxParts;
-          chr = (chr + kTileKeys - 1) / kTileKeys * kTileKeys;
-          np = (len + chr - 1) / chr;
-        }
-        nparts = int(np);
+      if (pair_ok(q_offsets, kv_offsets, kv_rows, max_rows, r)) {
+        const int nsl = q_offsets[r + 1] - q_offsets[r];
+        const long long P = kv_offsets[r + 1] - kv_offsets[r];
+        const int passes = (nsl * G + kPassRows - 1) / kPassRows;
+        tiles = passes * ((nsl + kTileKeys - 1) / kTileKeys + int((P + kTileKeys - 1) / kTileKeys));
       }
     }
-    int tot_items, tot_rows, tot_cg;
-    const int ncg = nparts > 0 ? (rows + kCombineRows - 1) / kCombineRows : 0;
-    const int ib = item_run + block_exclusive_sum<kThreads>(nparts, s_scan, &tot_items);
-    const int rb = row_run + block_exclusive_sum<kThreads>(nparts * rows, s_scan, &tot_rows);
-    const int cb = cg_run + block_exclusive_sum<kThreads>(ncg, s_scan, &tot_cg);
+    int tot;
+    block_exclusive_sum<kThreads>(tiles, s_scan, &tot);
+    T += tot;
+  }
+  // pass B: units, the cut units and each workgroup's first unit
+  int unit_run = 0, tile_run = 0, cut_run = 0;
+  for (int base = 0; base < npairs; base += kThreads) {
+    const int pr = base + tid;
+    int passes = 0, per_pass = 0, nsl = 0, q0 = 0, ntail = 0, P = 0, kb = 0;
     if (pr < npairs) {
-      PairInfo pi;
-      pi.part_base = rb;
-      pi.nparts = nparts;
-      pi.q0 = q0;
-      pi.nslots = nsl;
-      ws.pairs[pr] = pi;
-      for (int i = 0; i < nparts; ++i) {
-        Item it;
-        it.pair = pr;
-        long long b = k0 + i * chr;
-        long long e = b + chr;
-        if (e > k0 + len) e = k0 + len;
-        it.kb = int(b);
-        it.ke = int(e);
-        it.part = i | (i == nparts - 1 ? (1 << 30) : 0);
-        ws.items[ib + i] = it;
+      const int r = pr / hkv;
+      if (pair_ok(q_offsets, kv_offsets, kv_rows, max_rows, r)) {
+        q0 = q_offsets[r];
+        nsl = q_offsets[r + 1] - q0;
+        kb = int(kv_offsets[r]);
+        P = int(kv_offsets[r + 1] - kv_offsets[r]);
+        passes = (nsl * G + kPassRows - 1) / kPassRows;
+        ntail = (nsl + kTileKeys - 1) / kTileKeys;
+        per_pass = ntail + (P + kTileKeys - 1) / kTileKeys;
       }
-      for (int c = 0; c < ncg; ++c) ws.cgroups[cb + c] = make_int2(pr, c * kCombineRows);
     }
-    item_run += tot_items;
-    row_run += tot_rows;
-    cg_run += tot_cg;
+    int tot_u, tot_t;
+    const int ub = unit_run + block_exclusive_sum<kThreads>(passes, s_scan, &tot_u);
+    const int tb = tile_run + block_exclusive_sum<kThreads>(passes * per_pass, s_scan, &tot_t);
+    // a unit is cut if two workgroup ranges share it
+    int ncut = 0;
+    for (int p = 0; p < passes; ++p) {
+      const long long ts = tb + p * per_pass, te = ts + per_pass;
+      if (range_of(ts, T, nb) != range_of(te - 1, T, nb)) ++ncut;
+    }
+    int tot_c;
+    const int cb = cut_run + block_exclusive_sum<kThreads>(ncut, s_scan, &tot_c);
+    int c = cb;
+    for (int p = 0; p < passes; ++p) {
+      Unit u;
+      u.tile_start = tb + p * per_pass;
+      u.tile_end = u.tile_start + per_pass;
+      u.q0 = q0;
+      u.nslots = nsl;
+      u.row0 = p * kPassRows;
+      u.rows = min(kPassRows, nsl * G - p * kPassRows);
+      u.kb = kb;
+      u.P = P;
+      u.kvh = pr % hkv;
+      u.ntail = ntail;
+      const int b0 = range_of(u.tile_start, T, nb), b1 = range_of(u.tile_end - 1, T, nb);
+      u.cut = b0 != b1;
+      u.pad = 0;
+      ws.units[ub + p] = u;
+      if (u.cut) {
+        Cut cu;
+        cu.unit = ub + p;
+        cu.b0 = b0;
+        cu.b1 = b1;
+        cu.first_slot = range_lo(T, b0, nb) < u.tile_start ? 1 : 0;
+        ws.cuts[c++] = cu;
+      }
+      // workgroups whose range starts inside this unit
+      int b = b0;
+      if (range_lo(T, b, nb) < u.tile_start) ++b;
+      for (; b <= b1; ++b) ws.wg_unit[b] = ub + p;
+    }
+    unit_run += tot_u;
+    tile_run += tot_t;
+    cut_run += tot_c;
   }
   if (tid == 0) {
-    ws.meta[0] = item_run;
-    ws.meta[1] = cg_run;
+    ws.meta[0] = unit_run;
+    ws.meta[1] = int(T);
+    ws.meta[2] = cut_run;
   }
 }
 
 // ---------------------------------------------------------------- main ----
-// LDS tile layout: 64 key rows x 256 bytes per tensor, no padding.  The 16-byte
+// LDS tile layout: 32 key rows x 256 bytes per tensor, no padding.  The 16-byte
 // chunk c of row r is stored at chunk position c ^ (r & 15), so that 16 rows
 // read at the same logical column fall into 16 different bank groups.
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef short shortx4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) shortx4 lds_shortx4_t;
 
-constexpr int kTileBytes = kTileKeys * kD * 2;  // 16 KB per tensor
+constexpr int kTileBytes = kTileKeys * kD * 2;  // 8 KB per tensor
 constexpr int kStageBytes = 2 * kTileBytes;     // K then V
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -206,26 +227,43 @@ __device__ __forceinline__ int swz(int row, int chunk) {
   return row * 256 + ((chunk ^ (row & 15)) << 4);
 }
 
-// Direct HBM -> LDS copy of one 64-key tile of K and V (each lane moves 16 bytes
-// per instruction, 1 KB = 4 rows per wave instruction).  Rows >= tn re-read row
-// tn-1 (in bounds); the softmax masks those keys.
+// One direct HBM -> LDS copy instruction: every lane moves 16 bytes from its
+// global address to lds_base + 16 * lane.  Issued through inline assembly so
+// that the compiler does not track it: its own bookkeeping would otherwise
+// drain every copy in flight before each LDS read.  Completion is awaited
+// explicitly (vmcnt) before a barrier in front of the reads.
+__device__ __forceinline__ void dma16(const void* src, const char* lds_dst) {
+  // the LDS destination is uniform in the wave; make that explicit for the SGPR operand
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(
+      uint32_t(reinterpret_cast<uintptr_t>((const lds_void_t*)lds_dst)));
+  uint32_t saved;  // M0 belongs to the compiler: restore it
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %2, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(src)
+      : "memory");
+}
+
+// Direct HBM -> LDS copy of one 32-key tile of K and V: 16 wave instructions of
+// 1 KB (4 rows; each lane moves 16 bytes).  Rows >= tn re-read row tn-1 (in
+// bounds); the softmax masks those keys.
 template <int NW>
 __device__ __forceinline__ void issue_tile(char* stage, const uint16_t* kbase,
                                            const uint16_t* vbase, size_t stride, int tn) {
-  constexpr int kLoads = 32 / NW;
+  constexpr int kLoads = 16 / NW;
   const int lane = threadIdx.x & (kWave - 1);
   const int wid = threadIdx.x / kWave;
 #pragma unroll
   for (int j = 0; j < kLoads; ++j) {
-    const int q = wid * kLoads + j;  // 0..31, uniform in the wave
-    const int tensor = q >> 4;
-    const int rg = q & 15;
+    const int q = wid * kLoads + j;  // 0..15, uniform in the wave
+    const int tensor = q >> 3;
+    const int rg = q & 7;
     const int row = rg * 4 + (lane >> 4);
     const int c = (lane & 15) ^ (row & 15);
     const int srow = row < tn ? row : tn - 1;
     const uint16_t* src = (tensor ? vbase : kbase) + size_t(srow) * stride + c * 8;
-    __builtin_amdgcn_global_load_lds(src, (lds_void_t*)(stage + tensor * kTileBytes + rg * 1024),
-                                     16, 0, 0);
+    dma16(src, stage + tensor * kTileBytes + rg * 1024);
   }
 }
 
@@ -236,6 +274,15 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt(imm);
 }
 
+// Wait until at most n * L vector-memory operations of this wave are in flight.
+template <int L>
+__device__ __forceinline__ void wait_vm_tiles(int n) {
+  if (n >= 3) wait_vm<3 * L>();
+  else if (n == 2) wait_vm<2 * L>();
+  else if (n == 1) wait_vm<L>();
+  else wait_vm<0>();
+}
+
 struct RowTile {
   floatx4 o[8];  // O^T: lane holds dims 16*dt + 4*(lane/16) + i of row lane%16
   float m;       // running max of scaled logits (log2 units)
@@ -243,10 +290,10 @@ struct RowTile {
 };
 
 // Per-lane LDS byte offsets of the swizzled fragment reads (lane constants; the
-// subtile / key-block parts are compile-time immediates on top of these).
+// second 16-key subtile is +4096 bytes on top of these).
 struct LaneOffsets {
-  int k[4];  // K A-fragment of chunk 4*kk + lg, row lr of a 16-key subtile
-  int v[8];  // V^T transposed read of dims 16*dt + 4*(lr&3), key 4*lg + (lr>>2) of a 16-key block
+  int k[4];  // K A-fragment: chunk 4*kk + lg of row lr
+  int v[8];  // V^T transposed read: dims 16*dt + 4*(lr&3) of key 4*lg + (lr>>2)
 };
 
 __device__ __forceinline__ LaneOffsets lane_offsets() {
@@ -264,60 +311,88 @@ __device__ __forceinline__ LaneOffsets lane_offsets() {
   return o;
 }
 
-// One 64-key tile from LDS against the wave's row tiles.
-// masked: keys >= tn are invisible, and key j is visible to a row only if bit j
-// (of this tile's 64) is set in its mask words.
-template <int MT>
+// Reductions over the four lanes that hold one row (lanes l, l^16, l^32, l^48)
+// with the gfx950 row/half swaps instead of LDS permutes.
+__device__ __forceinline__ float row_max4(float v) {
+  const uint32_t u = __float_as_uint(v);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const uint32_t w = __float_as_uint(v);
+  const auto b = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+__device__ __forceinline__ float row_sum4(float v) {
+  const uint32_t u = __float_as_uint(v);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const uint32_t w = __float_as_uint(v);
+  const auto b = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// One 32-key tile from LDS against the wave's first NT row tiles.  masked: keys
+// >= tn are invisible, and key j is visible to a row only if bit j of its mask
+// word is set.  All LDS reads are issued up front and the independent MFMA
+// chains are interleaved, so LDS and MFMA latencies overlap.
+template <int NT>
 __device__ __forceinline__ void compute_tile(const char* kt, const char* vt, const bf16x8 (*qf)[4],
-                                             RowTile* rt, int ntiles, bool masked, int tn,
-                                             float scale2, const uint32_t (*mword)[2],
-                                             const LaneOffsets& lo) {
+                                             RowTile* rt, bool masked, int tn, float scale2,
+                                             const uint32_t* mword, const LaneOffsets& lo) {
   const int lane = threadIdx.x & (kWave - 1);
   const int lg = lane >> 4;
-  // S^T = K Q^T for the 4 subtiles of 16 keys (subtile s4 = rows 16*s4.., +4096 bytes)
-  floatx4 st[MT][4];
+  bf16x8 kf[2][4];
 #pragma unroll
-  for (int s4 = 0; s4 < 4; ++s4) {
-    bf16x8 kf[4];
+  for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk)
-      kf[kk] = *reinterpret_cast<const bf16x8*>(kt + lo.k[kk] + 4096 * s4);
+      kf[s2][kk] = *reinterpret_cast<const bf16x8*>(kt + lo.k[kk] + 4096 * s2);
+  // S^T = K Q^T: 2 subtiles x NT row tiles of independent accumulation chains
+  floatx4 st[NT][2];
 #pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      if (t >= ntiles) break;
-      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kk], qf[t][kk], acc, 0, 0, 0);
-      st[t][s4] = acc;
-    }
+    for (int s2 = 0; s2 < 2; ++s2) st[t][s2] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        st[t][s2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s2][kk], qf[t][kk], st[t][s2], 0, 0, 0);
+  // V^T fragments via transposed LDS reads (input lane i of block lg reads 4 dims of
+  // one key, output lane j gets dim j of 4 keys); their latency hides under the softmax
+  bf16x8 vf[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) {
+    char* base = const_cast<char*>(vt) + lo.v[dt];
+    const shortx4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(base));
+    const shortx4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(base + 4096));
+    vf[dt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
   }
-  // online softmax (base 2); lane holds keys 16*s4 + 4*lg + i of row lane%16
-  bf16x8 pf[MT][2];
+  // online softmax (base 2); lane holds keys 16*s2 + 4*lg + i of row lane%16
+  bf16x8 pf[NT];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) {
-    if (t >= ntiles) break;
-    float sv[16];
+  for (int t = 0; t < NT; ++t) {
+    float sv[8];
 #pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4)
+    for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) sv[4 * s4 + i] = st[t][s4][i];
+      for (int i = 0; i < 4; ++i) sv[4 * s2 + i] = st[t][s2][i];
     if (masked) {
-      // key >> 5 == s4 >> 1 because 4 * lg + i < 16
+      // key >> 5 == 0: one mask word covers the tile
 #pragma unroll
-      for (int s4 = 0; s4 < 4; ++s4)
+      for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = 16 * s4 + 4 * lg + i;
-          const bool ok = key < tn && ((mword[t][s4 >> 1] >> (key & 31)) & 1u);
-          sv[4 * s4 + i] = ok ? sv[4 * s4 + i] : -__builtin_inff();
+          const int key = 16 * s2 + 4 * lg + i;
+          const bool ok = key < tn && ((mword[t] >> key) & 1u);
+          sv[4 * s2 + i] = ok ? sv[4 * s2 + i] : -__builtin_inff();
         }
     }
-    float mx = sv[0];
-#pragma unroll
-    for (int e = 1; e < 16; ++e) mx = fmaxf(mx, sv[e]);
-    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    float mx = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
+                     fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
+    mx = row_max4(mx);
     const float mt = mx * scale2;  // -inf stays -inf
     const float m_new = fmaxf(rt[t].m, mt);
     if (__ballot(m_new > rt[t].m) != 0ull) {
@@ -330,256 +405,275 @@ __device__ __forceinline__ void compute_tile(const char* kt, const char* vt, con
     const float neg_m = m_new == -__builtin_inff() ? 0.0f : -m_new;
     float psum = 0.0f;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
+    for (int e = 0; e < 8; ++e) {
       sv[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[e], scale2, neg_m));
       psum += sv[e];
     }
     rt[t].l += psum;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      uint4 pk;
-      pk.x = pack_bf16x2(sv[8 * h + 0], sv[8 * h + 1]);
-      pk.y = pack_bf16x2(sv[8 * h + 2], sv[8 * h + 3]);
-      pk.z = pack_bf16x2(sv[8 * h + 4], sv[8 * h + 5]);
-      pk.w = pack_bf16x2(sv[8 * h + 6], sv[8 * h + 7]);
-      pf[t][h] = as_bf16x8(pk);
-    }
+    uint4 pk;
+    pk.x = pack_bf16x2(sv[0], sv[1]);
+    pk.y = pack_bf16x2(sv[2], sv[3]);
+    pk.z = pack_bf16x2(sv[4], sv[5]);
+    pk.w = pack_bf16x2(sv[6], sv[7]);
+    pf[t] = as_bf16x8(pk);
   }
-  // O^T += V^T P^T.  V^T fragment via transposed LDS reads: input lane i of block lg
-  // reads 4 dims of one key, output lane j gets dim j of 4 keys.
+  // O^T += V^T P^T
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) {
+  for (int dt = 0; dt < 8; ++dt)
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      char* base = const_cast<char*>(vt) + lo.v[dt] + 8192 * h;  // keys 32h.. (+16 keys = 4096 B)
-      const shortx4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(base));
-      const shortx4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(base + 4096));
-      const bf16x8 vf =
-          __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-      for (int t = 0; t < MT; ++t) {
-        if (t >= ntiles) break;
-        rt[t].o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[t][h], rt[t].o[dt], 0, 0, 0);
-      }
-    }
-  }
+    for (int t = 0; t < NT; ++t)
+      rt[t].o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pf[t], rt[t].o[dt], 0, 0, 0);
 }
 
 template <int NW, int MT, int STAGES>
-__global__ __launch_bounds__(NW * kWave) void attn_main_kernel(
+__global__ __launch_bounds__(NW * kWave, 8 / NW) void attn_main_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_new,
     const uint16_t* __restrict__ v_new, const uint16_t* __restrict__ k_cache,
     const uint16_t* __restrict__ v_cache, const uint32_t* __restrict__ tree_mask, int W, int hq,
-    int hkv, int G, float scale2, AttnWs ws) {
+    int hkv, int G, float scale2, AttnWs ws, float* __restrict__ out, float* __restrict__ lse) {
   __shared__ __attribute__((aligned(1024))) char s_ring[STAGES * kStageBytes];
-  constexpr int kLoads = 32 / NW;
-  constexpr int kRowsPerPass = NW * MT * 16;
+  constexpr int kLoads = 16 / NW;
+  static_assert(STAGES >= 2 && STAGES <= 4, "ring depth");
+  static_assert(NW * MT * 16 == kPassRows && MT == 2, "rows per unit");
 
-  const int n_items = ws.meta[0];
-  if (int(blockIdx.x) >= n_items) return;
-  const Item it = ws.items[blockIdx.x];
-  const PairInfo pi = ws.pairs[it.pair];
-  const int kvh = it.pair % hkv;
-  const bool last = (it.part >> 30) & 1;
-  const int part = it.part & ((1 << 30) - 1);
-  const int rows = pi.nslots * G;
+  const int nb = gridDim.x;
+  const int b = blockIdx.x;
+  const long long T = ws.meta[1];
+  const int lo = int(range_lo(T, b, nb));
+  const int hi = int(range_lo(T, b + 1, nb));
+  if (lo >= hi) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int wid = threadIdx.x / kWave;
   const int lr = lane & 15, lg = lane >> 4;
   const size_t stride = size_t(hkv) * kD;
-  const int ntk = (it.ke - it.kb + kTileKeys - 1) / kTileKeys;
-  const uint16_t* kpre = k_cache + size_t(it.kb) * stride + kvh * kD;
-  const uint16_t* vpre = v_cache + size_t(it.kb) * stride + kvh * kD;
-  const LaneOffsets lo = lane_offsets();
+  const LaneOffsets lof = lane_offsets();
 
-  for (int pass = 0; pass * kRowsPerPass < rows; ++pass) {
-    int ntiles = 0;
-    bf16x8 qf[MT][4];
-    RowTile rt[MT];
-    int rho_t[MT];
-#pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      const int tile = pass * NW * MT + wid + NW * t;
-      const int rho = tile * 16 + lr;
-      rho_t[t] = rho;
-      if (tile * 16 < rows) ntiles = t + 1;
-      uint4 qv[4] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0),
-                     make_uint4(0, 0, 0, 0)};
-      if (rho < rows) {
-        const uint16_t* qrow = q + (size_t(pi.q0 + rho / G) * hq + kvh * G + rho % G) * kD;
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
-          qv[kk] = *reinterpret_cast<const uint4*>(qrow + 32 * kk + 8 * lg);
-      }
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) qf[t][kk] = as_bf16x8(qv[kk]);
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) rt[t].o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-      rt[t].m = -__builtin_inff();
-      rt[t].l = 0.0f;
+  // issue side of the ring: unit of the next tile to copy
+  const int nunits = ws.meta[0];
+  int iu = ws.wg_unit[b];
+  Unit iud = ws.units[iu];
+  auto issue = [&](int u) {
+    while (u >= iud.tile_end && iu + 1 < nunits) iud = ws.units[++iu];
+    const int lt = u - iud.tile_start;
+    if (lt < 0 || u >= iud.tile_end) return;  // unreachable: units tile [0, T) contiguously
+    const uint16_t *kb, *vb;
+    int tn;
+    if (lt < iud.ntail) {
+      const size_t row = size_t(iud.q0) + size_t(lt) * kTileKeys;
+      kb = k_new + row * stride + iud.kvh * kD;
+      vb = v_new + row * stride + iud.kvh * kD;
+      tn = min(kTileKeys, iud.nslots - lt * kTileKeys);
+    } else {
+      const int pt = lt - iud.ntail;
+      const size_t row = size_t(iud.kb) + size_t(pt) * kTileKeys;
+      kb = k_cache + row * stride + iud.kvh * kD;
+      vb = v_cache + row * stride + iud.kvh * kD;
+      tn = min(kTileKeys, iud.P - pt * kTileKeys);
     }
-    wait_vm<0>();  // Q (and earlier stores) done: vmcnt now counts tile copies only
+    issue_tile<NW>(s_ring + (u % STAGES) * kStageBytes, kb, vb, stride, tn);
+  };
 
-    // The item's tiles: the prefix chunk through a STAGES-deep ring of LDS tiles,
-    // then (last chunk only) the tree tail, one synchronous tile at a time.
-    const int ntail = last ? (pi.nslots + kTileKeys - 1) / kTileKeys : 0;
-    uint32_t mword[MT][2];
+  // compute side: the unit of the current tile and the wave's rows in it
+  int cu = iu;
+  Unit cud = iud;
+  int ntiles = 0;
+  bf16x8 qf[MT][4];
+  RowTile rt[MT];
+  int rho_t[MT];
+  uint32_t mw[MT][kMaskWords];
+  int mw0 = 0;  // tail tile of mw[.][0]
+
+  // ring prologue
 #pragma unroll
-    for (int s = 0; s < STAGES - 1; ++s)
-      if (s < ntk)
-        issue_tile<NW>(s_ring + s * kStageBytes, kpre + size_t(s) * kTileKeys * stride,
-                       vpre + size_t(s) * kTileKeys * stride, stride,
-                       min(kTileKeys, it.ke - it.kb - s * kTileKeys));
-    for (int i = 0; i < ntk + ntail; ++i) {
-      const char* stg;
-      int tn;
-      if (i < ntk) {
-        const int ahead = min(STAGES - 2, ntk - 1 - i);  // tiles issued after tile i
-        if (ahead >= 2) wait_vm<2 * kLoads>();
-        else if (ahead == 1) wait_vm<kLoads>();
-        else wait_vm<0>();
-        __syncthreads();
-        const int nx = i + STAGES - 1;
-        if (nx < ntk)
-          issue_tile<NW>(s_ring + (nx % STAGES) * kStageBytes,
-                         kpre + size_t(nx) * kTileKeys * stride,
-                         vpre + size_t(nx) * kTileKeys * stride, stride,
-                         min(kTileKeys, it.ke - it.kb - nx * kTileKeys));
-        stg = s_ring + (i % STAGES) * kStageBytes;
-        tn = min(kTileKeys, it.ke - it.kb - i * kTileKeys);
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (lo + s < hi) issue(lo + s);
+
+  for (int t = lo; t < hi; ++t) {
+    wait_vm_tiles<kLoads>(min(STAGES - 2, hi - 1 - t));  // tile t has landed
+    __syncthreads();  // ... for every wave, and tile t-1 is no longer read
+    while (t >= cud.tile_end && cu + 1 < nunits) cud = ws.units[++cu];
+    const int lt = t - cud.tile_start;
+    const bool seg_start = (t == lo) || (lt == 0);
+    if (t + STAGES - 1 < hi) issue(t + STAGES - 1);
+    if (seg_start) {
+      // Q fragments of this wave's row tiles, the tree-tail mask words, fresh state.
+      // Loaded after the ring copy above and awaited with vmcnt(0): afterwards no
+      // compiler-visible load is outstanding, so the steady-state tiles carry no
+      // implicit wait that would drain the ring.
+      ntiles = 0;
 #pragma unroll
-        for (int t = 0; t < MT; ++t) mword[t][0] = mword[t][1] = 0xFFFFFFFFu;
-      } else {
-        // tree tail: the request's own slots, visible through the ancestor bitmask
-        const int j0 = (i - ntk) * kTileKeys;
-        tn = min(kTileKeys, pi.nslots - j0);
-        __syncthreads();  // every wave is done with the previous tile's stage
-        issue_tile<NW>(s_ring, k_new + size_t(pi.q0 + j0) * stride + kvh * kD,
-                       v_new + size_t(pi.q0 + j0) * stride + kvh * kD, stride, tn);
+      for (int i = 0; i < MT; ++i) {
+        const int tile = wid + NW * i;
+        const int rho = tile * 16 + lr;  // row within the unit
+        rho_t[i] = rho;
+        if (tile * 16 < cud.rows) ntiles = i + 1;
+        uint4 qv[4] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0),
+                       make_uint4(0, 0, 0, 0)};
+        const int ra = cud.row0 + rho;  // row within the pair
+        if (rho < cud.rows) {
+          const uint16_t* qrow = q + (size_t(cud.q0 + ra / G) * hq + cud.kvh * G + ra % G) * kD;
 #pragma unroll
-        for (int t = 0; t < MT; ++t) {
-          mword[t][0] = 0u;
-          mword[t][1] = 0u;
-          if (rho_t[t] < rows) {
-            const uint32_t* mrow = tree_mask + size_t(pi.q0 + rho_t[t] / G) * W;
-            const int w0 = j0 >> 5;
-            if (w0 < W) mword[t][0] = mrow[w0];
-            if (w0 + 1 < W) mword[t][1] = mrow[w0 + 1];
-          }
+          for (int kk = 0; kk < 4; ++kk)
+            qv[kk] = *reinterpret_cast<const uint4*>(qrow + 32 * kk + 8 * lg);
+        }
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) qf[i][kk] = as_bf16x8(qv[kk]);
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) rt[i].o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+        rt[i].m = -__builtin_inff();
+        rt[i].l = 0.0f;
+        mw0 = lt;
+#pragma unroll
+        for (int k = 0; k < kMaskWords; ++k) {
+          const int word = lt + k;
+          mw[i][k] = (rho < cud.rows && word < cud.ntail && word < W)
+                         ? tree_mask[size_t(cud.q0 + ra / G) * W + word]
+                         : 0u;
+        }
+      }
+      wait_vm<0>();
+    }
+    // this tile: tree tail (masked by the ancestor bits) or KV prefix
+    const char* stg = s_ring + (t % STAGES) * kStageBytes;
+    bool masked;
+    int tn;
+    uint32_t word[MT];
+    if (lt < cud.ntail) {
+      tn = min(kTileKeys, cud.nslots - lt * kTileKeys);
+      masked = true;
+      const int k = lt - mw0;
+      if (k < kMaskWords) {
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+          uint32_t w = 0u;
+#pragma unroll
+          for (int kk = 0; kk < kMaskWords; ++kk) w = (kk == k) ? mw[i][kk] : w;
+          word[i] = w;
+        }
+      } else {  // requests with more than 128 verify slots: fetch the word now
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+          const int ra = cud.row0 + rho_t[i];
+          word[i] = (rho_t[i] < cud.rows && lt < W) ? tree_mask[size_t(cud.q0 + ra / G) * W + lt]
+                                                     : 0u;
         }
         wait_vm<0>();
-        __syncthreads();
-        stg = s_ring;
       }
-      if (ntiles > 0)
-        compute_tile<MT>(stg, stg + kTileBytes, qf, rt, ntiles, tn < kTileKeys || i >= ntk, tn,
-                         scale2, mword, lo);
+    } else {
+      tn = min(kTileKeys, cud.P - (lt - cud.ntail) * kTileKeys);
+      masked = tn < kTileKeys;
+#pragma unroll
+      for (int i = 0; i < MT; ++i) word[i] = 0xFFFFFFFFu;
     }
-    __syncthreads();
-    // partial results of this chunk
+    if (ntiles == MT)
+      compute_tile<MT>(stg, stg + kTileBytes, qf, rt, masked, tn, scale2, word, lof);
+    else if (ntiles > 0)
+      compute_tile<1>(stg, stg + kTileBytes, qf, rt, masked, tn, scale2, word, lof);
+
+    if (t + 1 == hi || t + 1 == cud.tile_end) {
+      // end of this workgroup's segment of the unit: final output or a partial
+      const int slot = lo < cud.tile_start ? 1 : 0;
 #pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      if (t >= ntiles) break;
-      float l = rt[t].l;
-      l += __shfl_xor(l, 16, kWave);
-      l += __shfl_xor(l, 32, kWave);
-      const int rho = rho_t[t];
-      if (rho < rows) {
-        const size_t prow = size_t(pi.part_base) + size_t(part) * rows + rho;
-        float* po = ws.part_o + prow * kD;
+      for (int i = 0; i < MT; ++i) {
+        if (i >= ntiles) break;
+        const float l = row_sum4(rt[i].l);
+        const int rho = rho_t[i];
+        if (rho < cud.rows) {
+          if (!cud.cut) {
+            const int ra = cud.row0 + rho;
+            const size_t orow = size_t(cud.q0 + ra / G) * hq + cud.kvh * G + ra % G;
+            const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+            float* po = out + orow * kD;
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt)
-          *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = rt[t].o[dt];
-        if (lg == 0) {
-          ws.part_ml[prow * 2 + 0] = rt[t].m;
-          ws.part_ml[prow * 2 + 1] = l;
+            for (int dt = 0; dt < 8; ++dt)
+              *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = rt[i].o[dt] * inv;
+            if (lse != nullptr && lg == 0)
+              lse[orow] = l > 0.0f ? (rt[i].m + log2f(l)) * kLn2 : -__builtin_inff();
+          } else {
+            const size_t prow = (size_t(2 * b + slot)) * kPassRows + rho;
+            float* po = ws.part_o + prow * kD;
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt)
+              *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = rt[i].o[dt];
+            if (lg == 0) {
+              ws.part_ml[prow * 2 + 0] = rt[i].m;
+              ws.part_ml[prow * 2 + 1] = l;
+            }
+          }
         }
       }
+      wait_vm<0>();  // stores drained: later waits count tile copies only
     }
   }
 }
 
 // ------------------------------------------------------------- combine ----
-// One workgroup per group of 8 rows of one pair; thread = (row, 4 dims).  All
-// chunk partials of a row are loaded independently, then merged in chunk order.
-__global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv, int G, AttnWs ws,
+// One workgroup per cut unit; thread = (row, 4 dims).  The unit's partials are
+// merged in workgroup order.
+__global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int G, AttnWs ws,
                                                                 float* __restrict__ out,
                                                                 float* __restrict__ lse) {
-  if (int(blockIdx.x) >= ws.meta[1]) return;
-  const int2 cg = ws.cgroups[blockIdx.x];
-  const PairInfo pi = ws.pairs[cg.x];
-  const int kvh = cg.x % hkv;
-  const int rows = pi.nslots * G;
-  const int rho = cg.y + (threadIdx.x >> 5);
-  const int d4 = (threadIdx.x & 31) * 4;
-  if (rho >= rows) return;
-  float mv[kMaxParts], lv[kMaxParts];
-  float M = -__builtin_inff();
-#pragma unroll
-  for (int i = 0; i < kMaxParts; ++i) {
-    mv[i] = -__builtin_inff();
-    lv[i] = 0.0f;
-    if (i < pi.nparts) {
-      const size_t prow = size_t(pi.part_base) + size_t(i) * rows + rho;
+  if (int(blockIdx.x) >= ws.meta[2]) return;
+  const Cut c = ws.cuts[blockIdx.x];
+  const Unit u = ws.units[c.unit];
+  const long long T = ws.meta[1];
+  const int nb = gridDim.x;  // the main kernel's workgroup count
+  // workgroups with an empty range (fewer tiles than workgroups) left no partial
+  auto live = [&](int bb) { return range_lo(T, bb, nb) < range_lo(T, bb + 1, nb); };
+  for (int e = threadIdx.x; e < u.rows * (kD / 4); e += kThreads) {
+    const int rho = e / (kD / 4);
+    const int d4 = (e % (kD / 4)) * 4;
+    float M = -__builtin_inff();
+    for (int bb = c.b0; bb <= c.b1; ++bb) {
+      if (!live(bb)) continue;
+      const size_t prow = size_t(2 * bb + (bb == c.b0 ? c.first_slot : 0)) * kPassRows + rho;
+      M = fmaxf(M, ws.part_ml[prow * 2]);
+    }
+    const float Mu = M == -__builtin_inff() ? 0.0f : M;
+    float L = 0.0f;
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int bb = c.b0; bb <= c.b1; ++bb) {
+      if (!live(bb)) continue;
+      const size_t prow = size_t(2 * bb + (bb == c.b0 ? c.first_slot : 0)) * kPassRows + rho;
       const float2 ml = *reinterpret_cast<const float2*>(ws.part_ml + prow * 2);
-      mv[i] = ml.x;
-      lv[i] = ml.y;
-      M = fmaxf(M, ml.x);
+      const float w = __builtin_amdgcn_exp2f(ml.x - Mu);
+      L += w * ml.y;
+      acc += w * *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
     }
+    const int ra = u.row0 + rho;
+    const size_t orow = size_t(u.q0 + ra / G) * hq + u.kvh * G + ra % G;
+    const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+    *reinterpret_cast<floatx4*>(out + orow * kD + d4) = acc * inv;
+    if (lse != nullptr && d4 == 0) lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
   }
-  const float Mu = M == -__builtin_inff() ? 0.0f : M;
-  float L = 0.0f;
-  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int i = 0; i < kMaxParts; ++i) {
-    if (i < pi.nparts) {
-      const size_t prow = size_t(pi.part_base) + size_t(i) * rows + rho;
-      const float w = __builtin_amdgcn_exp2f(mv[i] - Mu);
-      L += w * lv[i];
-      const floatx4 v = *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
-      acc += w * v;
-    }
-  }
-  const int slot = pi.q0 + rho / G;
-  const int head = kvh * G + rho % G;
-  float* orow = out + (size_t(slot) * hq + head) * kD + d4;
-  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
-  *reinterpret_cast<floatx4*>(orow) = acc * inv;
-  if (lse != nullptr && d4 == 0)
-    lse[size_t(slot) * hq + head] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
 }
 
-int target_items_for_device() { return 8 * device_cu_count(); }
+int main_workgroups() { return 2 * device_cu_count(); }
 
 }  // namespace
 
 size_t attn_workspace_bytes(int32_t R, int32_t max_rows, int32_t hq, int32_t hkv) {
-  const size_t icap = item_capacity(R, hkv, target_items_for_device());
-  const size_t cgcap = cgroup_capacity(R, max_rows, hq, hkv);
-  const size_t part_rows = size_t(kMaxParts) * max_rows * hq;
-  return 256 + al(icap * sizeof(Item)) + al(size_t(R) * hkv * sizeof(PairInfo)) +
-         al(cgcap * sizeof(int2)) + al(part_rows * 2 * sizeof(float)) +
-         al(part_rows * kD * sizeof(float));
+  return attn_ws_total(unit_capacity(R, max_rows, hq, hkv), main_workgroups());
 }
 
 int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
-  const int target = target_items_for_device();
-  const size_t icap = item_capacity(a.R, a.hkv, target);
-  const size_t cgcap = cgroup_capacity(a.R, a.max_rows, a.hq, a.hkv);
-  const size_t part_rows = size_t(kMaxParts) * a.max_rows * a.hq;
-  AttnWs ws = attn_layout(a.workspace, a.R, a.hkv, icap, cgcap, part_rows);
+  (void)hipGetLastError();  // clear errors left by unrelated runtime calls
+  const int nb = main_workgroups();
+  const size_t ucap = unit_capacity(a.R, a.max_rows, a.hq, a.hkv);
+  AttnWs ws = attn_layout(a.workspace, ucap, nb);
   const int G = a.hq / a.hkv;
   hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kThreads), 0, stream, a.q_offsets,
                      a.kv_offsets, static_cast<long long>(a.kv_rows), a.R, a.hkv, G, a.max_rows,
-                     target, ws, a.status);
+                     nb, ws, a.status);
   const bool prof = g_attn_ev_start != nullptr && g_attn_ev_stop != nullptr;
   if (prof && hipEventRecord(g_attn_ev_start, stream) != hipSuccess) return ECHO_ERR_HIP;
-  hipLaunchKernelGGL((attn_main_kernel<kMainWaves, kMT, kStages>), dim3(unsigned(icap)),
+  hipLaunchKernelGGL((attn_main_kernel<kMainWaves, kMT, kStages>), dim3(unsigned(nb)),
                      dim3(kMainWaves * kWave), 0, stream, a.q, a.k_new, a.v_new, a.k_cache,
-                     a.v_cache, a.tree_mask, a.mask_words, a.hq, a.hkv, G, a.sm_scale * kLog2e, ws);
+                     a.v_cache, a.tree_mask, a.mask_words, a.hq, a.hkv, G, a.sm_scale * kLog2e, ws,
+                     a.out, a.lse);
   if (prof && hipEventRecord(g_attn_ev_stop, stream) != hipSuccess) return ECHO_ERR_HIP;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(cgcap)), dim3(kCombineRows * 32), 0,
-                     stream, a.hq, a.hkv, G, ws, a.out, a.lse);
+  hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(nb)), dim3(kThreads), 0, stream, a.hq, G,
+                     ws, a.out, a.lse);
   return hipGetLastError() == hipSuccess ? ECHO_OK : ECHO_ERR_HIP;
 }
 

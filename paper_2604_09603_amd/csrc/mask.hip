@@ -192,6 +192,7 @@ int32_t launch_build_tree_mask(const int32_t* cand_offsets, const int32_t* paren
                                int32_t* slot_parent, int32_t* slot_token, int32_t* position_ids,
                                uint32_t* tree_mask, int32_t mask_words, int32_t* status,
                                hipStream_t stream) {
+  (void)hipGetLastError();  // clear errors left by unrelated runtime calls
   const size_t lds = mask_lds_bytes(R, budget);
   const bool aligned = (reinterpret_cast<uintptr_t>(selected) & 15u) == 0;
   auto kern = aligned ? mask_kernel<true> : mask_kernel<false>;
