@@ -1,24 +1,34 @@
 // Tree-masked grouped-query verification attention (one verification forward
 // over the flattened super-tree).  Three launches:
 //
-//   attn_plan     one workgroup.  The work is a stream of 32-key tiles: for each
-//                 (request, kv head) pair and each 128-row pass over its rows
-//                 (rows = verify slots x query heads of the GQA group), first
-//                 the tree-tail tiles (the new keys of the request's own slots)
-//                 and then the KV-prefix tiles.  The stream is cut into equal
-//                 contiguous ranges, one per workgroup of the main kernel; the
-//                 plan records each unit's tiles and which units are cut.
-//   attn_main     persistent, two workgroups (4 waves each) per CU.  Each
-//                 workgroup streams its range HBM -> LDS through a 4-stage
-//                 ring of direct-to-LDS copies that runs across unit
-//                 boundaries; every tile is shared by all rows of its unit.
-//                 S^T = K Q^T and O^T = V^T P^T on v_mfma_f32_16x16x32_bf16
-//                 (fp32 accumulation), online softmax in base 2, ancestor
-//                 bitmask on tree-tail tiles.  A unit that lies inside one
-//                 range is normalised and written to out/lse directly; a cut
-//                 unit leaves one partial (O, max, sum) per workgroup.
-//   attn_combine  one workgroup per cut unit: merges its partials in range
-//                 order (deterministic) into out and lse.
+//   attn_plan     one workgroup.  A stream is one KV head of one request
+//                 together with a pass over its rows (rows = verify slots x
+//                 query heads of the GQA group, at most 48 per pass).  The
+//                 streams of a request are grouped four at a time, head-major;
+//                 a group is one unit of work whose tiles are the request's
+//                 32-key tiles: first the tree-tail tiles (the new keys of the
+//                 request's own slots), then the KV-prefix tiles.  The tiles of
+//                 all units are cut into equal contiguous ranges, one per
+//                 workgroup of the main kernel; the plan records each unit's
+//                 tiles and which units are cut.
+//   attn_main     persistent, one workgroup of four waves per CU.  Wave w runs
+//                 stream w of every unit in its workgroup's range over the same
+//                 tiles as its three siblings: it copies its head's slice of
+//                 each tile HBM -> LDS into its own two-stage ring with
+//                 direct-to-LDS loads, reads the tile into registers, refills
+//                 the stage and multiplies the tile against all rows of its
+//                 stream.  The four waves read the four heads of the same token
+//                 rows at the same time (whole rows of the KV cache), and the
+//                 passes of one head share their reads in the caches.  No
+//                 barrier is needed: every wave owns its ring and its softmax
+//                 state.  S^T = K Q^T and O^T = V^T P^T on
+//                 v_mfma_f32_16x16x32_bf16 (fp32 accumulation), online softmax
+//                 in base 2, ancestor bitmask on tree-tail tiles.  A unit that
+//                 lies inside one range is normalised and written to out/lse; a
+//                 cut unit leaves one partial (O, max, sum) per stream and
+//                 workgroup.
+//   attn_combine  one thread per (cut unit, stream, row, 4 dims): merges the
+//                 partials in range order (deterministic) into out and lse.
 #include "echo_device.h"
 #include "echo_internal.h"
 
@@ -27,25 +37,30 @@ namespace {
 
 constexpr int kD = ECHO_HEAD_DIM;   // 128
 constexpr int kThreads = 256;       // plan / combine workgroups
-constexpr int kMainWaves = 4;       // main kernel: waves per workgroup (two workgroups per CU)
-constexpr int kMT = 2;              // 16-row tiles per wave
-constexpr int kPassRows = kMainWaves * kMT * 16;  // rows per unit (128)
-constexpr int kStages = 4;          // LDS ring depth (32-key K+V tiles, 16 KB each)
+constexpr int kWaves = 4;           // main kernel: waves (streams) per workgroup, one per CU
+constexpr int kMaxMT = 3;           // 16-row tiles per stream (more would spill registers)
+constexpr int kPassRows = kMaxMT * 16;  // rows per stream (48)
+constexpr int kWaveStages = 2;      // per-wave LDS ring depth (32-key K+V tiles)
 constexpr int kTileKeys = 32;       // keys per tile
-constexpr int kMaskWords = 4;       // tree-tail mask words preloaded per unit (128 slots)
+constexpr int kMaskWords = 2;       // tree-tail mask words preloaded per row and segment
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+// The softmax reference max is raised only when a logit exceeds it by more than
+// 2^8 (in the exponent): probabilities stay <= 256, exact after normalisation.
+constexpr float kRescaleSlack = 8.0f;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-// One unit of the tile stream: a row pass of one (request, kv head) pair.
+// One unit of the tile stream: a group of four streams of one request.
+// Stream s = 4 * group + w runs KV head s / passes over the rows of pass
+// s % passes; s >= hkv * passes is empty.
 struct Unit {
   int32_t tile_start, tile_end;  // global tile range: ntail tail tiles, then prefix tiles
   int32_t q0, nslots;            // the request's verify slots
-  int32_t row0, rows;            // rows [row0, row0 + rows) of the pair (slot-major, G per slot)
   int32_t kb, P;                 // KV prefix rows [kb, kb + P)
-  int32_t kvh, ntail;            // kv head; ceil(nslots / 32)
+  int32_t ntail, passes;         // ceil(nslots / 32); row passes per KV head
+  int32_t rpp, group;            // rows per pass (the last pass may have fewer); stream group
   int32_t cut, pad;              // cut: covered by more than one workgroup
 };
 
@@ -54,18 +69,24 @@ struct Cut {
 };
 
 struct AttnWs {
-  int32_t* meta;   // [0] = units, [1] = tiles, [2] = cut units
+  int32_t* meta;   // [0] units, [1] tiles, [2] cut units, [3] workgroups with work
   Unit* units;
   int32_t* wg_unit;  // [nb] unit holding each workgroup's first tile
   Cut* cuts;
-  float* part_ml;  // [2 * nb * 128][2]: running max (log2 units), sum
-  float* part_o;   // [2 * nb * 128][128]
+  float* part_ml;  // [2 * nb * 4 * 48][2]: softmax reference max (log2 units), sum
+  float* part_o;   // [2 * nb * 4 * 48][128]
 };
 
 __host__ __device__ inline size_t al(size_t x) { return (x + 255) / 256 * 256; }
 
+// Units never exceed one per request plus one per four streams.
 __host__ inline size_t unit_capacity(int R, int max_rows, int hq, int hkv) {
-  return size_t(R) * hkv + (size_t(max_rows) * hq + kPassRows - 1) / kPassRows;
+  const size_t passes = size_t(R) + (size_t(max_rows) * (hq / hkv) + kPassRows - 1) / kPassRows;
+  return size_t(R) + (size_t(hkv) * passes + kWaves - 1) / kWaves;
+}
+
+__host__ __device__ inline size_t part_rows(int nb) {
+  return size_t(2) * nb * kWaves * kPassRows;
 }
 
 __host__ __device__ inline AttnWs attn_layout(void* base, size_t ucap, int nb) {
@@ -80,117 +101,160 @@ __host__ __device__ inline AttnWs attn_layout(void* base, size_t ucap, int nb) {
   w.cuts = reinterpret_cast<Cut*>(p);
   p += al(size_t(nb) * sizeof(Cut));
   w.part_ml = reinterpret_cast<float*>(p);
-  p += al(size_t(2) * nb * kPassRows * 2 * sizeof(float));
+  p += al(part_rows(nb) * 2 * sizeof(float));
   w.part_o = reinterpret_cast<float*>(p);
   return w;
 }
 
 __host__ inline size_t attn_ws_total(size_t ucap, int nb) {
   return 256 + al(ucap * sizeof(Unit)) + al(size_t(nb) * 4) + al(size_t(nb) * sizeof(Cut)) +
-         al(size_t(2) * nb * kPassRows * 2 * 4) + al(size_t(2) * nb * kPassRows * kD * 4);
+         al(part_rows(nb) * 2 * 4) + al(part_rows(nb) * kD * 4);
 }
 
-// First tile of workgroup b when T tiles are cut into nb equal ranges.
-__device__ __forceinline__ long long range_lo(long long T, int b, int nb) { return T * b / nb; }
+// Partial row of (workgroup b, slot, stream w, row rho).
+__device__ __forceinline__ size_t part_row(int b, int slot, int w, int rho) {
+  return (size_t(2 * b + slot) * kWaves + w) * kPassRows + rho;
+}
+
+// First tile of workgroup b when T tiles are cut into nw equal ranges (nw <= T).
+__device__ __forceinline__ long long range_lo(long long T, int b, int nw) { return T * b / nw; }
 // Workgroup whose range holds tile t.
-__device__ __forceinline__ int range_of(long long t, long long T, int nb) {
-  return int(((t + 1) * nb + T - 1) / T) - 1;
+__device__ __forceinline__ int range_of(long long t, long long T, int nw) {
+  return int(((t + 1) * nw + T - 1) / T) - 1;
+}
+
+// The rows of stream w of a unit: KV head, first row and row count (rows == 0:
+// the stream is empty).
+struct Stream {
+  int kvh, row0, rows;
+};
+
+__device__ __forceinline__ Stream stream_of(const Unit& u, int w, int hkv, int G) {
+  Stream s = {0, 0, 0};
+  const int id = kWaves * u.group + w;
+  if (u.passes <= 0 || id >= hkv * u.passes) return s;
+  s.kvh = id / u.passes;
+  s.row0 = (id % u.passes) * u.rpp;
+  s.rows = min(u.rpp, u.nslots * G - s.row0);
+  return s;
 }
 
 // ---------------------------------------------------------------- plan ----
-__device__ __forceinline__ bool pair_ok(const int32_t* q_offsets, const int64_t* kv_offsets,
-                                        long long kv_rows, int max_rows, int r) {
+__device__ __forceinline__ bool request_ok(const int32_t* q_offsets, const int64_t* kv_offsets,
+                                           long long kv_rows, int max_rows, int r) {
   const int q0 = q_offsets[r], q1 = q_offsets[r + 1];
   const long long k0 = kv_offsets[r], k1 = kv_offsets[r + 1];
   return q0 >= 0 && q1 >= q0 && q1 <= max_rows && k0 >= 0 && k1 >= k0 && k1 <= kv_rows;
 }
 
+struct RequestShape {
+  int groups, tiles, q0, nsl, kb, P, ntail, passes, rpp;
+};
+
+// A request's rows per head split into passes of at most 48 rows, as even as
+// possible; its hkv * passes streams form ceil(/4) groups over the same tiles.
+__device__ __forceinline__ RequestShape request_shape(const int32_t* q_offsets,
+                                                      const int64_t* kv_offsets,
+                                                      long long kv_rows, int max_rows, int R,
+                                                      int hkv, int G, int r) {
+  RequestShape s = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+  if (r >= R || !request_ok(q_offsets, kv_offsets, kv_rows, max_rows, r)) return s;
+  s.q0 = q_offsets[r];
+  s.nsl = q_offsets[r + 1] - s.q0;
+  s.kb = int(kv_offsets[r]);
+  s.P = int(kv_offsets[r + 1] - kv_offsets[r]);
+  const int rows = s.nsl * G;
+  s.passes = (rows + kPassRows - 1) / kPassRows;
+  if (s.passes == 0) return s;
+  s.rpp = (rows + s.passes - 1) / s.passes;
+  s.ntail = (s.nsl + kTileKeys - 1) / kTileKeys;
+  s.groups = (hkv * s.passes + kWaves - 1) / kWaves;
+  s.tiles = s.ntail + (s.P + kTileKeys - 1) / kTileKeys;
+  return s;
+}
+
 __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
     const int32_t* __restrict__ q_offsets, const int64_t* __restrict__ kv_offsets,
-    long long kv_rows, int R, int hkv, int G, int max_rows, int nb, AttnWs ws, int32_t* status) {
+    long long kv_rows, int R, int hkv, int G, int max_rows, int nb, long long ucap, AttnWs ws,
+    int32_t* status) {
   __shared__ int s_scan[kThreads / kWave + 1];
   const int tid = threadIdx.x;
-  const int npairs = R * hkv;
   int bits = 0;
   for (int r = tid; r < R; r += kThreads)
-    if (!pair_ok(q_offsets, kv_offsets, kv_rows, max_rows, r)) bits |= ECHO_DATA_BAD_OFFSETS;
-  wave_status_or(status, bits);
+    if (!request_ok(q_offsets, kv_offsets, kv_rows, max_rows, r)) bits |= ECHO_DATA_BAD_OFFSETS;
 
-  // pass A: total tiles
-  long long T = 0;
-  for (int base = 0; base < npairs; base += kThreads) {
-    const int pr = base + tid;
-    int tiles = 0;
-    if (pr < npairs) {
-      const int r = pr / hkv;
-      if (pair_ok(q_offsets, kv_offsets, kv_rows, max_rows, r)) {
-        const int nsl = q_offsets[r + 1] - q_offsets[r];
-        const long long P = kv_offsets[r + 1] - kv_offsets[r];
-        const int passes = (nsl * G + kPassRows - 1) / kPassRows;
-        tiles = passes * ((nsl + kTileKeys - 1) / kTileKeys + int((P + kTileKeys - 1) / kTileKeys));
-      }
-    }
-    int tot;
-    block_exclusive_sum<kThreads>(tiles, s_scan, &tot);
-    T += tot;
+  // pass A: total units and tiles
+  long long T = 0, U = 0;
+  for (int base = 0; base < R; base += kThreads) {
+    const RequestShape s =
+        request_shape(q_offsets, kv_offsets, kv_rows, max_rows, R, hkv, G, base + tid);
+    int tot_u, tot_t;
+    block_exclusive_sum<kThreads>(s.groups, s_scan, &tot_u);
+    block_exclusive_sum<kThreads>(s.groups * s.tiles, s_scan, &tot_t);
+    U += tot_u;
+    T += tot_t;
   }
+  // slot ranges that overlap (a non-monotone CSR) could ask for more units than
+  // the workspace holds, and tile indices are 32-bit: then nothing is scheduled
+  if (U > ucap || T > 0x7FFFFFFFll) {
+    if (tid == 0) {
+      bits |= ECHO_DATA_BAD_OFFSETS;
+      ws.meta[0] = 0;
+      ws.meta[1] = 0;
+      ws.meta[2] = 0;
+      ws.meta[3] = 0;
+    }
+    wave_status_or(status, bits);
+    return;
+  }
+  wave_status_or(status, bits);
+  // workgroups with work: never more than tiles, so that no range is empty
+  const int nw = T < nb ? int(T) : nb;
   // pass B: units, the cut units and each workgroup's first unit
   int unit_run = 0, tile_run = 0, cut_run = 0;
-  for (int base = 0; base < npairs; base += kThreads) {
-    const int pr = base + tid;
-    int passes = 0, per_pass = 0, nsl = 0, q0 = 0, ntail = 0, P = 0, kb = 0;
-    if (pr < npairs) {
-      const int r = pr / hkv;
-      if (pair_ok(q_offsets, kv_offsets, kv_rows, max_rows, r)) {
-        q0 = q_offsets[r];
-        nsl = q_offsets[r + 1] - q0;
-        kb = int(kv_offsets[r]);
-        P = int(kv_offsets[r + 1] - kv_offsets[r]);
-        passes = (nsl * G + kPassRows - 1) / kPassRows;
-        ntail = (nsl + kTileKeys - 1) / kTileKeys;
-        per_pass = ntail + (P + kTileKeys - 1) / kTileKeys;
-      }
-    }
+  for (int base = 0; base < R; base += kThreads) {
+    const RequestShape s =
+        request_shape(q_offsets, kv_offsets, kv_rows, max_rows, R, hkv, G, base + tid);
     int tot_u, tot_t;
-    const int ub = unit_run + block_exclusive_sum<kThreads>(passes, s_scan, &tot_u);
-    const int tb = tile_run + block_exclusive_sum<kThreads>(passes * per_pass, s_scan, &tot_t);
+    const int ub = unit_run + block_exclusive_sum<kThreads>(s.groups, s_scan, &tot_u);
+    const int tb = tile_run + block_exclusive_sum<kThreads>(s.groups * s.tiles, s_scan, &tot_t);
     // a unit is cut if two workgroup ranges share it
     int ncut = 0;
-    for (int p = 0; p < passes; ++p) {
-      const long long ts = tb + p * per_pass, te = ts + per_pass;
-      if (range_of(ts, T, nb) != range_of(te - 1, T, nb)) ++ncut;
+    for (int g = 0; g < s.groups; ++g) {
+      const long long ts = tb + g * s.tiles, te = ts + s.tiles;
+      if (range_of(ts, T, nw) != range_of(te - 1, T, nw)) ++ncut;
     }
     int tot_c;
     const int cb = cut_run + block_exclusive_sum<kThreads>(ncut, s_scan, &tot_c);
     int c = cb;
-    for (int p = 0; p < passes; ++p) {
+    for (int g = 0; g < s.groups; ++g) {
       Unit u;
-      u.tile_start = tb + p * per_pass;
-      u.tile_end = u.tile_start + per_pass;
-      u.q0 = q0;
-      u.nslots = nsl;
-      u.row0 = p * kPassRows;
-      u.rows = min(kPassRows, nsl * G - p * kPassRows);
-      u.kb = kb;
-      u.P = P;
-      u.kvh = pr % hkv;
-      u.ntail = ntail;
-      const int b0 = range_of(u.tile_start, T, nb), b1 = range_of(u.tile_end - 1, T, nb);
+      u.tile_start = tb + g * s.tiles;
+      u.tile_end = u.tile_start + s.tiles;
+      u.q0 = s.q0;
+      u.nslots = s.nsl;
+      u.kb = s.kb;
+      u.P = s.P;
+      u.ntail = s.ntail;
+      u.passes = s.passes;
+      u.rpp = s.rpp;
+      u.group = g;
+      const int b0 = range_of(u.tile_start, T, nw), b1 = range_of(u.tile_end - 1, T, nw);
       u.cut = b0 != b1;
       u.pad = 0;
-      ws.units[ub + p] = u;
+      ws.units[ub + g] = u;
       if (u.cut) {
         Cut cu;
-        cu.unit = ub + p;
+        cu.unit = ub + g;
         cu.b0 = b0;
         cu.b1 = b1;
-        cu.first_slot = range_lo(T, b0, nb) < u.tile_start ? 1 : 0;
+        cu.first_slot = range_lo(T, b0, nw) < u.tile_start ? 1 : 0;
         ws.cuts[c++] = cu;
       }
       // workgroups whose range starts inside this unit
       int b = b0;
-      if (range_lo(T, b, nb) < u.tile_start) ++b;
-      for (; b <= b1; ++b) ws.wg_unit[b] = ub + p;
+      if (range_lo(T, b, nw) < u.tile_start) ++b;
+      for (; b <= b1; ++b) ws.wg_unit[b] = ub + g;
     }
     unit_run += tot_u;
     tile_run += tot_t;
@@ -200,6 +264,7 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
     ws.meta[0] = unit_run;
     ws.meta[1] = int(T);
     ws.meta[2] = cut_run;
+    ws.meta[3] = nw;
   }
 }
 
@@ -213,6 +278,8 @@ typedef __attribute__((address_space(3))) shortx4 lds_shortx4_t;
 
 constexpr int kTileBytes = kTileKeys * kD * 2;  // 8 KB per tensor
 constexpr int kStageBytes = 2 * kTileBytes;     // K then V
+constexpr int kMainLds = kWaves * kWaveStages * kStageBytes;  // 128 KB
+static_assert(kMainLds <= 160 * 1024, "gfx950 LDS per workgroup");
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -227,43 +294,73 @@ __device__ __forceinline__ int swz(int row, int chunk) {
   return row * 256 + ((chunk ^ (row & 15)) << 4);
 }
 
-// One direct HBM -> LDS copy instruction: every lane moves 16 bytes from its
-// global address to lds_base + 16 * lane.  Issued through inline assembly so
-// that the compiler does not track it: its own bookkeeping would otherwise
-// drain every copy in flight before each LDS read.  Completion is awaited
-// explicitly (vmcnt) before a barrier in front of the reads.
-__device__ __forceinline__ void dma16(const void* src, const char* lds_dst) {
+// One direct HBM -> LDS copy instruction: every lane moves 16 bytes from
+// base + voff (base uniform in the wave, voff per lane) to lds_dst + 16 * lane.
+// Issued through inline assembly so that the compiler does not track it: its
+// own bookkeeping would otherwise drain every copy in flight before each LDS
+// read.  Completion is awaited explicitly (vmcnt).
+__device__ __forceinline__ uint64_t uniform64(uint64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(x));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(x >> 32));
+  return (uint64_t(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ void dma16(uint64_t base, uint32_t voff, const char* lds_dst) {
   // the LDS destination is uniform in the wave; make that explicit for the SGPR operand
   const uint32_t lds = __builtin_amdgcn_readfirstlane(
       uint32_t(reinterpret_cast<uintptr_t>((const lds_void_t*)lds_dst)));
+  const uint64_t sbase = uniform64(base);
   uint32_t saved;  // M0 belongs to the compiler: restore it
   asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %2, off\n\t"
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %2, %3\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "s"(lds), "v"(src)
+      : "s"(lds), "v"(voff), "s"(sbase)
       : "memory");
 }
 
-// Direct HBM -> LDS copy of one 32-key tile of K and V: 16 wave instructions of
-// 1 KB (4 rows; each lane moves 16 bytes).  Rows >= tn re-read row tn-1 (in
-// bounds); the softmax masks those keys.
-template <int NW>
-__device__ __forceinline__ void issue_tile(char* stage, const uint16_t* kbase,
-                                           const uint16_t* vbase, size_t stride, int tn) {
-  constexpr int kLoads = 16 / NW;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int wid = threadIdx.x / kWave;
+constexpr int kCopiesPerTile = 16;  // wave instructions of 1 KB (4 key rows) per K+V tile
+
+// Per-lane source offsets of one tile copy: instruction j (per tensor) fills LDS
+// rows 4j .. 4j+3; the lane fetches the source chunk that the swizzle puts at
+// its LDS position.
+__device__ __forceinline__ int copy_row(int j) { return j * 4 + ((threadIdx.x & (kWave - 1)) >> 4); }
+__device__ __forceinline__ uint32_t copy_chunk16(int row) {
+  return uint32_t(((threadIdx.x & 15) ^ (row & 15)) * 16);
+}
+
+struct CopyPlan {
+  uint32_t off[8];  // byte offset from the tile's first key row (full tile)
+};
+
+__device__ __forceinline__ CopyPlan copy_plan(uint32_t row_bytes) {
+  CopyPlan cp;
 #pragma unroll
-  for (int j = 0; j < kLoads; ++j) {
-    const int q = wid * kLoads + j;  // 0..15, uniform in the wave
-    const int tensor = q >> 3;
-    const int rg = q & 7;
-    const int row = rg * 4 + (lane >> 4);
-    const int c = (lane & 15) ^ (row & 15);
-    const int srow = row < tn ? row : tn - 1;
-    const uint16_t* src = (tensor ? vbase : kbase) + size_t(srow) * stride + c * 8;
-    dma16(src, stage + tensor * kTileBytes + rg * 1024);
+  for (int j = 0; j < 8; ++j) {
+    const int row = copy_row(j);
+    cp.off[j] = uint32_t(row) * row_bytes + copy_chunk16(row);
+  }
+  return cp;
+}
+
+// Copy one K+V tile (tn <= 32 valid key rows, rows row_bytes apart) into a
+// stage.  Rows >= tn re-read row tn-1 (in bounds); the softmax masks those keys.
+__device__ __forceinline__ void issue_tile(char* stage, uint64_t kbase, uint64_t vbase,
+                                           uint32_t row_bytes, int tn, const CopyPlan& cp) {
+  if (tn == kTileKeys) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dma16(kbase, cp.off[j], stage + j * 1024);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dma16(vbase, cp.off[j], stage + kTileBytes + j * 1024);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int row = copy_row(j);
+      const int srow = row < tn ? row : tn - 1;
+      const uint32_t off = uint32_t(srow) * row_bytes + copy_chunk16(row);
+      dma16(kbase, off, stage + j * 1024);
+      dma16(vbase, off, stage + kTileBytes + j * 1024);
+    }
   }
 }
 
@@ -274,18 +371,14 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt(imm);
 }
 
-// Wait until at most n * L vector-memory operations of this wave are in flight.
-template <int L>
-__device__ __forceinline__ void wait_vm_tiles(int n) {
-  if (n >= 3) wait_vm<3 * L>();
-  else if (n == 2) wait_vm<2 * L>();
-  else if (n == 1) wait_vm<L>();
-  else wait_vm<0>();
+__device__ __forceinline__ void wait_lds() {
+  // lgkmcnt(0); vmcnt and expcnt left at their maxima
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
 }
 
 struct RowTile {
   floatx4 o[8];  // O^T: lane holds dims 16*dt + 4*(lane/16) + i of row lane%16
-  float m;       // running max of scaled logits (log2 units)
+  float m;       // softmax reference max of scaled logits (log2 units)
   float l;       // this lane's share of the running sum
 };
 
@@ -331,26 +424,45 @@ __device__ __forceinline__ float row_sum4(float v) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
-// One 32-key tile from LDS against the wave's first NT row tiles.  masked: keys
-// >= tn are invisible, and key j is visible to a row only if bit j of its mask
-// word is set.  All LDS reads are issued up front and the independent MFMA
-// chains are interleaved, so LDS and MFMA latencies overlap.
-template <int NT>
-__device__ __forceinline__ void compute_tile(const char* kt, const char* vt, const bf16x8 (*qf)[4],
-                                             RowTile* rt, bool masked, int tn, float scale2,
-                                             const uint32_t* mword, const LaneOffsets& lo) {
-  const int lane = threadIdx.x & (kWave - 1);
-  const int lg = lane >> 4;
+// A whole 32-key tile in registers: the K A-fragments of both 16-key subtiles
+// and the V^T A-fragments of the eight 16-dim blocks.
+struct TileFrags {
   bf16x8 kf[2][4];
+  bf16x8 vf[8];
+};
+
+// Read a tile from its LDS stage.  V^T comes from transposed reads (input lane i
+// of block lg reads 4 dims of one key, output lane j gets dim j of 4 keys).
+__device__ __forceinline__ void load_tile(const char* kt, const char* vt, const LaneOffsets& lo,
+                                          TileFrags& f) {
 #pragma unroll
   for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk)
-      kf[s2][kk] = *reinterpret_cast<const bf16x8*>(kt + lo.k[kk] + 4096 * s2);
-  // S^T = K Q^T: 2 subtiles x NT row tiles of independent accumulation chains
-  floatx4 st[NT][2];
+      f.kf[s2][kk] = *reinterpret_cast<const bf16x8*>(kt + lo.k[kk] + 4096 * s2);
 #pragma unroll
-  for (int t = 0; t < NT; ++t)
+  for (int dt = 0; dt < 8; ++dt) {
+    char* base = const_cast<char*>(vt) + lo.v[dt];
+    const shortx4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(base));
+    const shortx4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(base + 4096));
+    f.vf[dt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+  }
+}
+
+// One 32-key tile (already in registers) against MT row tiles (all rows of the
+// unit).  masked: keys >= tn are invisible, and key j is visible to a row only
+// if bit j of its mask word is set.  The independent MFMA chains of the row
+// tiles and key subtiles are interleaved.
+template <int MT>
+__device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*qf)[4],
+                                             RowTile* rt, bool masked, int tn, float scale2,
+                                             const uint32_t* mword) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int lg = lane >> 4;
+  // S^T = K Q^T: 2 subtiles x MT row tiles of independent accumulation chains
+  floatx4 st[MT][2];
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) st[t][s2] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -358,22 +470,12 @@ __device__ __forceinline__ void compute_tile(const char* kt, const char* vt, con
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
-        st[t][s2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s2][kk], qf[t][kk], st[t][s2], 0, 0, 0);
-  // V^T fragments via transposed LDS reads (input lane i of block lg reads 4 dims of
-  // one key, output lane j gets dim j of 4 keys); their latency hides under the softmax
-  bf16x8 vf[8];
-#pragma unroll
-  for (int dt = 0; dt < 8; ++dt) {
-    char* base = const_cast<char*>(vt) + lo.v[dt];
-    const shortx4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(base));
-    const shortx4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4_t*)(base + 4096));
-    vf[dt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
-  }
+      for (int t = 0; t < MT; ++t)
+        st[t][s2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.kf[s2][kk], qf[t][kk], st[t][s2], 0, 0, 0);
   // online softmax (base 2); lane holds keys 16*s2 + 4*lg + i of row lane%16
-  bf16x8 pf[NT];
+  bf16x8 pf[MT];
 #pragma unroll
-  for (int t = 0; t < NT; ++t) {
+  for (int t = 0; t < MT; ++t) {
     float sv[8];
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2)
@@ -394,15 +496,16 @@ __device__ __forceinline__ void compute_tile(const char* kt, const char* vt, con
                      fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
     mx = row_max4(mx);
     const float mt = mx * scale2;  // -inf stays -inf
-    const float m_new = fmaxf(rt[t].m, mt);
-    if (__ballot(m_new > rt[t].m) != 0ull) {
-      const float alpha = __builtin_amdgcn_exp2f(rt[t].m - m_new);  // 0 for -inf, 1 if unchanged
+    // raise the reference only when a logit would exceed it by more than the slack
+    const bool grow = mt > rt[t].m + kRescaleSlack;
+    if (__ballot(grow) != 0ull) {
+      const float alpha = grow ? __builtin_amdgcn_exp2f(rt[t].m - mt) : 1.0f;  // 0 from -inf
       rt[t].l *= alpha;
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) rt[t].o[dt] *= alpha;
-      rt[t].m = m_new;
+      rt[t].m = grow ? mt : rt[t].m;
     }
-    const float neg_m = m_new == -__builtin_inff() ? 0.0f : -m_new;
+    const float neg_m = rt[t].m == -__builtin_inff() ? 0.0f : -rt[t].m;
     float psum = 0.0f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -421,234 +524,318 @@ __device__ __forceinline__ void compute_tile(const char* kt, const char* vt, con
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt)
 #pragma unroll
-    for (int t = 0; t < NT; ++t)
-      rt[t].o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pf[t], rt[t].o[dt], 0, 0, 0);
+    for (int t = 0; t < MT; ++t)
+      rt[t].o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.vf[dt], pf[t], rt[t].o[dt], 0, 0, 0);
 }
 
-template <int NW, int MT, int STAGES>
-__global__ __launch_bounds__(NW * kWave, 8 / NW) void attn_main_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_new,
-    const uint16_t* __restrict__ v_new, const uint16_t* __restrict__ k_cache,
-    const uint16_t* __restrict__ v_cache, const uint32_t* __restrict__ tree_mask, int W, int hq,
-    int hkv, int G, float scale2, AttnWs ws, float* __restrict__ out, float* __restrict__ lse) {
-  __shared__ __attribute__((aligned(1024))) char s_ring[STAGES * kStageBytes];
-  constexpr int kLoads = 16 / NW;
-  static_assert(STAGES >= 2 && STAGES <= 4, "ring depth");
-  static_assert(NW * MT * 16 == kPassRows && MT == 2, "rows per unit");
+// The wave's index in the workgroup, known to the compiler as wave-uniform (so
+// that everything derived from it stays in scalar registers).
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
+}
 
-  const int nb = gridDim.x;
-  const int b = blockIdx.x;
-  const long long T = ws.meta[1];
-  const int lo = int(range_lo(T, b, nb));
-  const int hi = int(range_lo(T, b + 1, nb));
-  if (lo >= hi) return;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int wid = threadIdx.x / kWave;
-  const int lr = lane & 15, lg = lane >> 4;
-  const size_t stride = size_t(hkv) * kD;
-  const LaneOffsets lof = lane_offsets();
+struct MainArgs {
+  const uint16_t* q;
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  const uint16_t* k_cache;
+  const uint16_t* v_cache;
+  const uint32_t* tree_mask;
+  int W, hq, hkv, G;
+  float scale2;
+  float* out;
+  float* lse;
+};
 
-  // issue side of the ring: unit of the next tile to copy
-  const int nunits = ws.meta[0];
-  int iu = ws.wg_unit[b];
-  Unit iud = ws.units[iu];
-  auto issue = [&](int u) {
-    while (u >= iud.tile_end && iu + 1 < nunits) iud = ws.units[++iu];
-    const int lt = u - iud.tile_start;
-    if (lt < 0 || u >= iud.tile_end) return;  // unreachable: units tile [0, T) contiguously
+// Unit descriptors are written by the plan launch and only read here: load
+// them through the constant address space (scalar loads when the index is
+// wave-uniform).
+typedef __attribute__((address_space(4))) const int32_t const_i32_t;
+__device__ __forceinline__ Unit load_unit(const Unit* units, int i) {
+  static_assert(sizeof(Unit) == 12 * sizeof(int32_t), "unit layout");
+  const_i32_t* p = (const_i32_t*)(units + i);
+  Unit u;
+  u.tile_start = p[0];
+  u.tile_end = p[1];
+  u.q0 = p[2];
+  u.nslots = p[3];
+  u.kb = p[4];
+  u.P = p[5];
+  u.ntail = p[6];
+  u.passes = p[7];
+  u.rpp = p[8];
+  u.group = p[9];
+  u.cut = p[10];
+  u.pad = p[11];
+  return u;
+}
+
+// Issue side of a wave's ring: the wave's k-th tile is lo + k; its copy goes to
+// stage k % 2 (nothing is copied where the wave's stream of the unit is empty).
+struct Issuer {
+  int iu;          // unit of the next tile to copy (wave-uniform)
+  Unit ud;
+  int k;           // ordinal of the next tile to copy
+  uint32_t copied;  // bit s: the last copy into stage s moved data
+};
+
+__device__ __forceinline__ void issue_next(Issuer& is, const MainArgs& a, const AttnWs& ws,
+                                           int nunits, int lo, int hi, int wid, char* ring,
+                                           const CopyPlan& cp) {
+  const int t = lo + is.k;
+  if (t >= hi) return;
+  while (t >= is.ud.tile_end && is.iu + 1 < nunits) {
+    is.iu = __builtin_amdgcn_readfirstlane(is.iu + 1);
+    is.ud = load_unit(ws.units, is.iu);
+  }
+  const int lt = t - is.ud.tile_start;
+  const Stream sm = stream_of(is.ud, wid, a.hkv, a.G);
+  const bool copy = sm.rows > 0 && lt >= 0 && t < is.ud.tile_end;
+  is.copied = (is.copied & ~(1u << (is.k & 1))) | (uint32_t(copy) << (is.k & 1));
+  if (copy) {
+    const size_t stride = size_t(a.hkv) * kD;
     const uint16_t *kb, *vb;
     int tn;
-    if (lt < iud.ntail) {
-      const size_t row = size_t(iud.q0) + size_t(lt) * kTileKeys;
-      kb = k_new + row * stride + iud.kvh * kD;
-      vb = v_new + row * stride + iud.kvh * kD;
-      tn = min(kTileKeys, iud.nslots - lt * kTileKeys);
+    if (lt < is.ud.ntail) {
+      const size_t row = size_t(is.ud.q0) + size_t(lt) * kTileKeys;
+      kb = a.k_new + row * stride + sm.kvh * kD;
+      vb = a.v_new + row * stride + sm.kvh * kD;
+      tn = min(kTileKeys, is.ud.nslots - lt * kTileKeys);
     } else {
-      const int pt = lt - iud.ntail;
-      const size_t row = size_t(iud.kb) + size_t(pt) * kTileKeys;
-      kb = k_cache + row * stride + iud.kvh * kD;
-      vb = v_cache + row * stride + iud.kvh * kD;
-      tn = min(kTileKeys, iud.P - pt * kTileKeys);
+      const int pt = lt - is.ud.ntail;
+      const size_t row = size_t(is.ud.kb) + size_t(pt) * kTileKeys;
+      kb = a.k_cache + row * stride + sm.kvh * kD;
+      vb = a.v_cache + row * stride + sm.kvh * kD;
+      tn = min(kTileKeys, is.ud.P - pt * kTileKeys);
     }
-    issue_tile<NW>(s_ring + (u % STAGES) * kStageBytes, kb, vb, stride, tn);
-  };
+    issue_tile(ring + (is.k & 1) * kStageBytes, reinterpret_cast<uint64_t>(kb),
+               reinterpret_cast<uint64_t>(vb), uint32_t(stride * 2), tn, cp);
+  }
+  ++is.k;
+}
 
-  // compute side: the unit of the current tile and the wave's rows in it
-  int cu = iu;
-  Unit cud = iud;
-  int ntiles = 0;
+// The tree-mask word of tail tile lt for a row of slot `slot` (0 outside).
+__device__ __forceinline__ uint32_t mask_word(const MainArgs& a, const Unit& ud, bool row_ok,
+                                              int slot, int lt) {
+  return (row_ok && lt >= 0 && lt < ud.ntail && lt < a.W)
+             ? a.tree_mask[size_t(slot) * a.W + lt]
+             : 0u;
+}
+
+// The wave's stream over one unit segment [seg_lo, seg_hi), then its output
+// (final or partial).
+template <int MT>
+__device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws, const Unit& ud,
+                                            const Stream& sm, int seg_lo, int seg_hi, int lo,
+                                            int hi, int nunits, int b, char* ring, Issuer& is,
+                                            const CopyPlan& cp, const LaneOffsets& lof) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wid = wave_id();
+  const int lr = lane & 15, lg = lane >> 4;
+  const int G = a.G;
+
+  // Q fragments of the stream's rows and the mask words of the segment's first
+  // tail tiles.  Loaded and awaited with vmcnt(0): afterwards no
+  // compiler-visible load is in flight, so the tile loop carries no implicit
+  // wait that would drain the ring.
+  const int lt0 = seg_lo - ud.tile_start;
   bf16x8 qf[MT][4];
-  RowTile rt[MT];
-  int rho_t[MT];
   uint32_t mw[MT][kMaskWords];
-  int mw0 = 0;  // tail tile of mw[.][0]
-
-  // ring prologue
+  RowTile rt[MT];
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (lo + s < hi) issue(lo + s);
-
-  for (int t = lo; t < hi; ++t) {
-    wait_vm_tiles<kLoads>(min(STAGES - 2, hi - 1 - t));  // tile t has landed
-    __syncthreads();  // ... for every wave, and tile t-1 is no longer read
-    while (t >= cud.tile_end && cu + 1 < nunits) cud = ws.units[++cu];
-    const int lt = t - cud.tile_start;
-    const bool seg_start = (t == lo) || (lt == 0);
-    if (t + STAGES - 1 < hi) issue(t + STAGES - 1);
-    if (seg_start) {
-      // Q fragments of this wave's row tiles, the tree-tail mask words, fresh state.
-      // Loaded after the ring copy above and awaited with vmcnt(0): afterwards no
-      // compiler-visible load is outstanding, so the steady-state tiles carry no
-      // implicit wait that would drain the ring.
-      ntiles = 0;
+  for (int i = 0; i < MT; ++i) {
+    const int rho = 16 * i + lr;
+    const int ra = sm.row0 + rho;
+    const bool row_ok = rho < sm.rows;
+    const int slot = ud.q0 + ra / G;
+    uint4 qv[4] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0),
+                   make_uint4(0, 0, 0, 0)};
+    if (row_ok) {
+      const uint16_t* qrow = a.q + (size_t(slot) * a.hq + sm.kvh * G + ra % G) * kD;
 #pragma unroll
-      for (int i = 0; i < MT; ++i) {
-        const int tile = wid + NW * i;
-        const int rho = tile * 16 + lr;  // row within the unit
-        rho_t[i] = rho;
-        if (tile * 16 < cud.rows) ntiles = i + 1;
-        uint4 qv[4] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0),
-                       make_uint4(0, 0, 0, 0)};
-        const int ra = cud.row0 + rho;  // row within the pair
-        if (rho < cud.rows) {
-          const uint16_t* qrow = q + (size_t(cud.q0 + ra / G) * hq + cud.kvh * G + ra % G) * kD;
-#pragma unroll
-          for (int kk = 0; kk < 4; ++kk)
-            qv[kk] = *reinterpret_cast<const uint4*>(qrow + 32 * kk + 8 * lg);
-        }
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) qf[i][kk] = as_bf16x8(qv[kk]);
-#pragma unroll
-        for (int dt = 0; dt < 8; ++dt) rt[i].o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-        rt[i].m = -__builtin_inff();
-        rt[i].l = 0.0f;
-        mw0 = lt;
-#pragma unroll
-        for (int k = 0; k < kMaskWords; ++k) {
-          const int word = lt + k;
-          mw[i][k] = (rho < cud.rows && word < cud.ntail && word < W)
-                         ? tree_mask[size_t(cud.q0 + ra / G) * W + word]
-                         : 0u;
-        }
-      }
-      wait_vm<0>();
+      for (int kk = 0; kk < 4; ++kk)
+        qv[kk] = *reinterpret_cast<const uint4*>(qrow + 32 * kk + 8 * lg);
     }
-    // this tile: tree tail (masked by the ancestor bits) or KV prefix
-    const char* stg = s_ring + (t % STAGES) * kStageBytes;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) qf[i][kk] = as_bf16x8(qv[kk]);
+#pragma unroll
+    for (int k = 0; k < kMaskWords; ++k) mw[i][k] = mask_word(a, ud, row_ok, slot, lt0 + k);
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) rt[i].o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    rt[i].m = -__builtin_inff();
+    rt[i].l = 0.0f;
+  }
+  wait_vm<0>();
+
+  for (int t = seg_lo; t < seg_hi; ++t) {
+    const int k = t - lo;  // tile ordinal of this wave
+    // tile k has landed once at most the copies of the next tile are in flight
+    if (is.k > k + 1 && ((is.copied >> ((k + 1) & 1)) & 1u)) wait_vm<kCopiesPerTile>();
+    else wait_vm<0>();
+    const char* stg = ring + (k & 1) * kStageBytes;
+    const int lt = t - ud.tile_start;
     bool masked;
     int tn;
     uint32_t word[MT];
-    if (lt < cud.ntail) {
-      tn = min(kTileKeys, cud.nslots - lt * kTileKeys);
+    if (lt < ud.ntail) {
+      tn = min(kTileKeys, ud.nslots - lt * kTileKeys);
       masked = true;
-      const int k = lt - mw0;
-      if (k < kMaskWords) {
+      if (lt - lt0 < kMaskWords) {
+#pragma unroll
+        for (int i = 0; i < MT; ++i) word[i] = (lt == lt0) ? mw[i][0] : mw[i][1];
+      } else {  // more than 64 verify slots in the segment's tail: fetch the word now
 #pragma unroll
         for (int i = 0; i < MT; ++i) {
-          uint32_t w = 0u;
-#pragma unroll
-          for (int kk = 0; kk < kMaskWords; ++kk) w = (kk == k) ? mw[i][kk] : w;
-          word[i] = w;
-        }
-      } else {  // requests with more than 128 verify slots: fetch the word now
-#pragma unroll
-        for (int i = 0; i < MT; ++i) {
-          const int ra = cud.row0 + rho_t[i];
-          word[i] = (rho_t[i] < cud.rows && lt < W) ? tree_mask[size_t(cud.q0 + ra / G) * W + lt]
-                                                     : 0u;
+          const int rho = 16 * i + lr;
+          const int ra = sm.row0 + rho;
+          word[i] = mask_word(a, ud, rho < sm.rows, ud.q0 + ra / G, lt);
         }
         wait_vm<0>();
       }
     } else {
-      tn = min(kTileKeys, cud.P - (lt - cud.ntail) * kTileKeys);
+      tn = min(kTileKeys, ud.P - (lt - ud.ntail) * kTileKeys);
       masked = tn < kTileKeys;
 #pragma unroll
       for (int i = 0; i < MT; ++i) word[i] = 0xFFFFFFFFu;
     }
-    if (ntiles == MT)
-      compute_tile<MT>(stg, stg + kTileBytes, qf, rt, masked, tn, scale2, word, lof);
-    else if (ntiles > 0)
-      compute_tile<1>(stg, stg + kTileBytes, qf, rt, masked, tn, scale2, word, lof);
+    // tile -> registers, then refill the stage at once: the ring stays full
+    // while the tile is multiplied
+    TileFrags f;
+    load_tile(stg, stg + kTileBytes, lof, f);
+    wait_lds();
+    issue_next(is, a, ws, nunits, lo, hi, wid, ring, cp);
+    compute_tile<MT>(f, qf, rt, masked, tn, a.scale2, word);
+  }
 
-    if (t + 1 == hi || t + 1 == cud.tile_end) {
-      // end of this workgroup's segment of the unit: final output or a partial
-      const int slot = lo < cud.tile_start ? 1 : 0;
+  // ---- output of the segment ----
+  const bool cut = ud.cut != 0;
+  const int slot_id = lo < ud.tile_start ? 1 : 0;
 #pragma unroll
-      for (int i = 0; i < MT; ++i) {
-        if (i >= ntiles) break;
-        const float l = row_sum4(rt[i].l);
-        const int rho = rho_t[i];
-        if (rho < cud.rows) {
-          if (!cud.cut) {
-            const int ra = cud.row0 + rho;
-            const size_t orow = size_t(cud.q0 + ra / G) * hq + cud.kvh * G + ra % G;
-            const float inv = l > 0.0f ? 1.0f / l : 0.0f;
-            float* po = out + orow * kD;
+  for (int i = 0; i < MT; ++i) {
+    const float L = row_sum4(rt[i].l);
+    const float M = rt[i].m;
+    const int rho = 16 * i + lr;
+    if (rho < sm.rows) {
+      if (!cut) {
+        const int ra = sm.row0 + rho;
+        const size_t orow = size_t(ud.q0 + ra / G) * a.hq + sm.kvh * G + ra % G;
+        const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+        float* po = a.out + orow * kD;
 #pragma unroll
-            for (int dt = 0; dt < 8; ++dt)
-              *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = rt[i].o[dt] * inv;
-            if (lse != nullptr && lg == 0)
-              lse[orow] = l > 0.0f ? (rt[i].m + log2f(l)) * kLn2 : -__builtin_inff();
-          } else {
-            const size_t prow = (size_t(2 * b + slot)) * kPassRows + rho;
-            float* po = ws.part_o + prow * kD;
+        for (int dt = 0; dt < 8; ++dt)
+          *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = rt[i].o[dt] * inv;
+        if (a.lse != nullptr && lg == 0)
+          a.lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
+      } else {
+        const size_t prow = part_row(b, slot_id, wid, rho);
+        float* po = ws.part_o + prow * kD;
 #pragma unroll
-            for (int dt = 0; dt < 8; ++dt)
-              *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = rt[i].o[dt];
-            if (lg == 0) {
-              ws.part_ml[prow * 2 + 0] = rt[i].m;
-              ws.part_ml[prow * 2 + 1] = l;
-            }
-          }
+        for (int dt = 0; dt < 8; ++dt)
+          *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = rt[i].o[dt];
+        if (lg == 0) {
+          ws.part_ml[prow * 2 + 0] = M;
+          ws.part_ml[prow * 2 + 1] = L;
         }
       }
-      wait_vm<0>();  // stores drained: later waits count tile copies only
     }
+  }
+  // stores drained: the ring's waits count tile copies only (stores may
+  // complete out of order with respect to the copies)
+  wait_vm<0>();
+}
+
+__global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a, AttnWs ws) {
+  __shared__ __attribute__((aligned(1024))) char smem[kMainLds];
+  const int b = blockIdx.x;
+  const int nw = ws.meta[3];
+  if (b >= nw) return;
+  const long long T = ws.meta[1];
+  const int lo = int(range_lo(T, b, nw));
+  const int hi = int(range_lo(T, b + 1, nw));
+  const int wid = wave_id();
+  const CopyPlan cp = copy_plan(uint32_t(a.hkv) * kD * 2);
+  const LaneOffsets lof = lane_offsets();
+  char* ring = smem + wid * (kWaveStages * kStageBytes);
+  const int nunits = ws.meta[0];
+
+  // the wave walks the units from the one holding the range's first tile; the
+  // issue side runs ahead of it
+  const int first_unit = __builtin_amdgcn_readfirstlane(ws.wg_unit[b]);
+  Issuer is;
+  is.iu = first_unit;
+  is.ud = load_unit(ws.units, is.iu);
+  is.k = 0;
+  is.copied = 0u;
+#pragma unroll
+  for (int s = 0; s < kWaveStages; ++s) issue_next(is, a, ws, nunits, lo, hi, wid, ring, cp);
+
+  int u = first_unit;
+  while (true) {
+    const Unit ud = load_unit(ws.units, u);
+    const int seg_lo = max(lo, ud.tile_start);
+    const int seg_hi = min(hi, ud.tile_end);
+    const Stream sm = stream_of(ud, wid, a.hkv, a.G);
+    const int mt = (sm.rows + 15) / 16;
+    if (mt == 0) {
+      // empty stream: nothing was copied for these tiles; keep the ring moving
+      for (int t = seg_lo; t < seg_hi; ++t) issue_next(is, a, ws, nunits, lo, hi, wid, ring, cp);
+    } else if (mt == 1) {
+      run_segment<1>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, is, cp, lof);
+    } else if (mt == 2) {
+      run_segment<2>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, is, cp, lof);
+    } else {
+      run_segment<3>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, is, cp, lof);
+    }
+    if (seg_hi >= hi || u + 1 >= nunits) break;
+    u = __builtin_amdgcn_readfirstlane(u + 1);
   }
 }
 
 // ------------------------------------------------------------- combine ----
-// One workgroup per cut unit; thread = (row, 4 dims).  The unit's partials are
-// merged in workgroup order.
-__global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int G, AttnWs ws,
+// One thread per (cut unit, stream, row, 4 dims); a cut's items span
+// kCombineBlocks workgroups.  The partials are merged in workgroup order.
+constexpr int kCombineItems = kWaves * kPassRows * (kD / 4);
+constexpr int kCombineBlocks = kCombineItems / kThreads;
+static_assert(kCombineItems % kThreads == 0, "combine tiling");
+
+__global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv, int G, AttnWs ws,
                                                                 float* __restrict__ out,
                                                                 float* __restrict__ lse) {
-  if (int(blockIdx.x) >= ws.meta[2]) return;
-  const Cut c = ws.cuts[blockIdx.x];
+  const int ci = blockIdx.x / kCombineBlocks;
+  if (ci >= ws.meta[2]) return;
+  const int e = (blockIdx.x % kCombineBlocks) * kThreads + threadIdx.x;
+  const int w = e / (kPassRows * (kD / 4));
+  const int rho = (e / (kD / 4)) % kPassRows;
+  const int d4 = (e % (kD / 4)) * 4;
+  const Cut c = ws.cuts[ci];
   const Unit u = ws.units[c.unit];
-  const long long T = ws.meta[1];
-  const int nb = gridDim.x;  // the main kernel's workgroup count
-  // workgroups with an empty range (fewer tiles than workgroups) left no partial
-  auto live = [&](int bb) { return range_lo(T, bb, nb) < range_lo(T, bb + 1, nb); };
-  for (int e = threadIdx.x; e < u.rows * (kD / 4); e += kThreads) {
-    const int rho = e / (kD / 4);
-    const int d4 = (e % (kD / 4)) * 4;
-    float M = -__builtin_inff();
-    for (int bb = c.b0; bb <= c.b1; ++bb) {
-      if (!live(bb)) continue;
-      const size_t prow = size_t(2 * bb + (bb == c.b0 ? c.first_slot : 0)) * kPassRows + rho;
-      M = fmaxf(M, ws.part_ml[prow * 2]);
-    }
-    const float Mu = M == -__builtin_inff() ? 0.0f : M;
-    float L = 0.0f;
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int bb = c.b0; bb <= c.b1; ++bb) {
-      if (!live(bb)) continue;
-      const size_t prow = size_t(2 * bb + (bb == c.b0 ? c.first_slot : 0)) * kPassRows + rho;
+  const Stream sm = stream_of(u, w, hkv, G);
+  if (rho >= sm.rows) return;
+  const int nparts = c.b1 - c.b0 + 1;
+  // partial of part i: workgroup b0 + i, whose segment may sit in its second slot
+  auto prow_of = [&](int i) { return part_row(c.b0 + i, i == 0 ? c.first_slot : 0, w, rho); };
+  float M = -__builtin_inff();
+  for (int i = 0; i < nparts; ++i) M = fmaxf(M, ws.part_ml[prow_of(i) * 2]);
+  float L = 0.0f;
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (M != -__builtin_inff()) {
+    for (int i = 0; i < nparts; ++i) {
+      const size_t prow = prow_of(i);
       const float2 ml = *reinterpret_cast<const float2*>(ws.part_ml + prow * 2);
-      const float w = __builtin_amdgcn_exp2f(ml.x - Mu);
-      L += w * ml.y;
-      acc += w * *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
+      if (ml.x == -__builtin_inff()) continue;
+      const float wgt = __builtin_amdgcn_exp2f(ml.x - M);
+      L += wgt * ml.y;
+      acc += wgt * *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
     }
-    const int ra = u.row0 + rho;
-    const size_t orow = size_t(u.q0 + ra / G) * hq + u.kvh * G + ra % G;
-    const float inv = L > 0.0f ? 1.0f / L : 0.0f;
-    *reinterpret_cast<floatx4*>(out + orow * kD + d4) = acc * inv;
-    if (lse != nullptr && d4 == 0) lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
   }
+  const int ra = sm.row0 + rho;
+  const size_t orow = size_t(u.q0 + ra / G) * hq + sm.kvh * G + ra % G;
+  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+  *reinterpret_cast<floatx4*>(out + orow * kD + d4) = acc * inv;
+  if (lse != nullptr && d4 == 0) lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
 }
 
-int main_workgroups() { return 2 * device_cu_count(); }
+int main_workgroups() { return device_cu_count(); }
 
 }  // namespace
 
@@ -664,16 +851,29 @@ int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
   const int G = a.hq / a.hkv;
   hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kThreads), 0, stream, a.q_offsets,
                      a.kv_offsets, static_cast<long long>(a.kv_rows), a.R, a.hkv, G, a.max_rows,
-                     nb, ws, a.status);
+                     nb, static_cast<long long>(ucap), ws, a.status);
+  MainArgs m;
+  m.q = a.q;
+  m.k_new = a.k_new;
+  m.v_new = a.v_new;
+  m.k_cache = a.k_cache;
+  m.v_cache = a.v_cache;
+  m.tree_mask = a.tree_mask;
+  m.W = a.mask_words;
+  m.hq = a.hq;
+  m.hkv = a.hkv;
+  m.G = G;
+  m.scale2 = a.sm_scale * kLog2e;
+  m.out = a.out;
+  m.lse = a.lse;
   const bool prof = g_attn_ev_start != nullptr && g_attn_ev_stop != nullptr;
   if (prof && hipEventRecord(g_attn_ev_start, stream) != hipSuccess) return ECHO_ERR_HIP;
-  hipLaunchKernelGGL((attn_main_kernel<kMainWaves, kMT, kStages>), dim3(unsigned(nb)),
-                     dim3(kMainWaves * kWave), 0, stream, a.q, a.k_new, a.v_new, a.k_cache,
-                     a.v_cache, a.tree_mask, a.mask_words, a.hq, a.hkv, G, a.sm_scale * kLog2e, ws,
-                     a.out, a.lse);
+  hipLaunchKernelGGL(attn_main_kernel, dim3(unsigned(nb)), dim3(kWaves * kWave), 0, stream, m,
+                     ws);
   if (prof && hipEventRecord(g_attn_ev_stop, stream) != hipSuccess) return ECHO_ERR_HIP;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(nb)), dim3(kThreads), 0, stream, a.hq, G,
-                     ws, a.out, a.lse);
+  // cut units number fewer than the main kernel's workgroups
+  hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(nb * kCombineBlocks)), dim3(kThreads), 0,
+                     stream, a.hq, a.hkv, G, ws, a.out, a.lse);
   return hipGetLastError() == hipSuccess ? ECHO_OK : ECHO_ERR_HIP;
 }
 
