@@ -21,21 +21,33 @@ import numpy as np
 from . import status as st
 
 
+def csr_ok(cand_offsets, N):
+    """A candidate CSR is usable iff it starts at 0, ends at N and never decreases.
+
+    This is the library boundary's convention, not the paper's: a malformed CSR
+    is a data error (BAD_OFFSETS), no candidate is scored and none is selected.
+    """
+    offs = np.asarray(cand_offsets, np.int64)
+    return int(offs[0]) == 0 and int(offs[-1]) == int(N) and bool(np.all(np.diff(offs) >= 0))
+
+
 def path_scores(cand_offsets, parent, logq):
     """S per candidate (float32), depth per candidate (root's children: 1), status.
 
     ``cand_offsets`` is the request-major CSR (R+1 entries); ``parent`` holds
     request-local indices (-1 = child of the root).  Clamps: NaN log q -> -inf,
     log q > 0 -> 0, parent outside [-1, local index) -> -1, depth > MAX_DEPTH ->
-    S = -inf.
+    S = -inf.  A malformed CSR (see ``csr_ok``) gives S = -inf everywhere.
     """
     offs = np.asarray(cand_offsets, np.int64)
     parent = np.asarray(parent, np.int32)
     logq = np.asarray(logq, np.float32)
-    N = int(offs[-1])
-    S = np.empty(N, np.float32)
-    depth = np.empty(N, np.int32)
+    N = len(logq)
+    S = np.full(N, -np.inf, np.float32)
+    depth = np.zeros(N, np.int32)
     status = 0
+    if not csr_ok(offs, N):
+        return S, depth, st.BAD_OFFSETS
     zero = np.float32(0.0)
     for r in range(len(offs) - 1):
         lo, hi = int(offs[r]), int(offs[r + 1])
@@ -92,6 +104,8 @@ def gate(cand_offsets, parent, logq, budget):
     """Full gate: returns dict(path_score, selected, num_selected, status)."""
     S, depth, status = path_scores(cand_offsets, parent, logq)
     sel = select_top_b(S, budget)
+    if not csr_ok(cand_offsets, len(S)):
+        return dict(path_score=S, depth=depth, selected=sel, num_selected=0, status=status)
     # ancestor closure: every selected node's parent is selected
     offs = np.asarray(cand_offsets, np.int64)
     par = clamped_parents(cand_offsets, parent)

@@ -20,12 +20,14 @@ If more than B candidates are selected, only the first B in ascending global
 index are packed (status OVER_CAPACITY).  A selected node whose parent is not
 selected is attached to its nearest selected ancestor (status NOT_CLOSED).
 Parent indices outside [-1, local index) met on those walks are read as -1
-(status BAD_PARENT).
+(status BAD_PARENT).  A malformed candidate CSR (not starting at 0, not ending
+at the candidate count, or decreasing) packs the roots only (status
+BAD_OFFSETS); that is the library boundary's convention.
 """
 import numpy as np
 
 from . import status as st
-from .gate import clamped_parents
+from .gate import clamped_parents, csr_ok
 
 
 def build_tree_mask(cand_offsets, parent, token, selected, root_token, prefix_len,
@@ -37,8 +39,15 @@ def build_tree_mask(cand_offsets, parent, token, selected, root_token, prefix_le
         raise ValueError("mask_words too small for budget + 1 slots")
     status = 0
     par_raw = np.asarray(parent, np.int32)
+    selected = np.asarray(selected)
+    if not csr_ok(offs, len(selected)):
+        # malformed candidate CSR: every request keeps its root slot only
+        status |= st.BAD_OFFSETS
+        selected = np.zeros(len(selected), np.uint8)
+        offs = np.zeros(R + 1, np.int64)
+        par_raw = np.full(len(selected), -1, np.int32)
     par = clamped_parents(offs, par_raw)
-    sel_idx = np.nonzero(np.asarray(selected) != 0)[0]
+    sel_idx = np.nonzero(selected != 0)[0]
     if len(sel_idx) > budget:
         status |= st.OVER_CAPACITY
         sel_idx = sel_idx[:budget]

@@ -96,6 +96,22 @@ def test_invalid_data_sets_status_bits():
     assert (res["status"] & 7) == 7
 
 
+@pytest.mark.parametrize("offs", [[2, 5, 9], [0, 6, 4, 9]])
+def test_malformed_candidate_csr(offs):
+    """A candidate CSR that does not start at 0 or decreases: nothing is scored or
+    packed, every request keeps its root slot, and BAD_OFFSETS is raised."""
+    offs = np.array(offs, np.int32)
+    R = len(offs) - 1
+    parent = np.array([-1, 0, 1, -1, 3, -1, 5, 6, -1], np.int32)
+    pool = dict(cand_offsets=offs, parent=parent, token=np.arange(9, dtype=np.int32) % 4,
+                logq=np.full(9, -0.5, np.float32), root_token=np.arange(R, dtype=np.int32))
+    print(f"[edges] malformed csr {offs.tolist()}", flush=True)
+    b = make_micro_batch(pool, 4, p_range=(3, 40))
+    res, ref = _check_all(b)
+    assert res["status"] & oracle.status.BAD_OFFSETS
+    assert res["num_slots"] == R
+
+
 def test_deep_chain_and_wide_mask():
     """A 20-deep chain (depth cap) plus 70 root children in another request (3 mask words)."""
     p1 = np.array([-1] + list(range(19)), np.int32)

@@ -124,3 +124,16 @@ def test_gate_invariants_on_presets(name):
     for g in np.random.default_rng(0).choice(len(S), 50, replace=False):
         e = bf.exact_path_score(offs, parent, logq, int(g))
         assert abs(float(S[g]) - float(e)) <= cfg.depth * abs(float(e)) * 2.0 ** -23
+
+
+@pytest.mark.parametrize("offs", [[2, 5, 9], [0, 6, 4, 9], [0, 4, 8]])
+def test_malformed_csr_scores_and_selects_nothing(offs):
+    """Boundary convention: a CSR that does not start at 0, end at N or rise is refused."""
+    N = 9
+    parent = np.array([-1, 0, 1, -1, 3, -1, 5, 6, -1], np.int32)
+    logq = np.full(N, -0.5, np.float32)
+    g = oracle.gate(np.array(offs, np.int32), parent, logq, 4)
+    assert g["status"] == oracle.status.BAD_OFFSETS
+    assert np.all(np.isneginf(g["path_score"]))
+    assert g["num_selected"] == 0 and not g["selected"].any()
+    assert oracle.gate(np.array([0, 3, 9], np.int32), parent, logq, 4)["num_selected"] == 4

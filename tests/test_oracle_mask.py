@@ -118,3 +118,17 @@ def test_mask_on_presets(name):
     assert res["status"] == 0
     assert res["num_slots"] == cfg.R + g["num_selected"]
     _check_against_dense(b, g["selected"], cfg.budget, res)
+
+
+def test_malformed_csr_packs_roots_only():
+    offs = np.array([0, 6, 4, 9], np.int32)          # decreasing: malformed
+    N = 9
+    selected = np.ones(N, np.uint8)
+    m = oracle.build_tree_mask(offs, np.full(N, -1, np.int32), np.arange(N, dtype=np.int32),
+                               selected, np.array([7, 8, 9], np.int32),
+                               np.array([3, 0, 5], np.int32), budget=4, mask_words=1)
+    assert m["status"] & oracle.status.BAD_OFFSETS
+    assert m["q_offsets"].tolist() == [0, 1, 2, 3]
+    assert m["slot_token"][:3].tolist() == [7, 8, 9]
+    assert m["position_ids"][:3].tolist() == [3, 0, 5]
+    assert m["tree_mask"][:3, 0].tolist() == [1, 1, 1]
