@@ -1,13 +1,17 @@
 // Greedy acceptance (standard SD, greedy decoding): per request, the deepest
 // verify slot whose whole root path matches the target argmax.  One wavefront
-// per request; each lane walks the parent chain of its slots (strictly
-// decreasing slot indices, so every walk ends), then a wave reduction picks
-// the deepest valid slot (ties: smallest local slot).
+// per request: the request's slot parents, tokens and targets are staged in LDS
+// in one round of loads (up to kStage slots; longer requests read memory),
+// each lane walks the parent chain of its slots (strictly decreasing slot
+// indices, so every walk ends), then a wave reduction picks the deepest valid
+// slot (ties: smallest local slot).
 #include "echo_device.h"
 #include "echo_internal.h"
 
 namespace echo {
 namespace {
+
+constexpr int kStage = 2048;  // slots per request staged in LDS
 
 __global__ __launch_bounds__(kWave) void accept_kernel(
     const int32_t* __restrict__ q_offsets, const int32_t* __restrict__ slot_parent,
@@ -26,19 +30,34 @@ __global__ __launch_bounds__(kWave) void accept_kernel(
     return;
   }
   const int n = q1 - q0;
+  __shared__ int32_t s_par[kStage];
+  __shared__ int32_t s_tok[kStage];
+  __shared__ int32_t s_tgt[kStage];
+  const bool staged = n <= kStage;
+  if (staged) {
+    for (int i = lane; i < n; i += kWave) {
+      s_par[i] = slot_parent[q0 + i];
+      s_tok[i] = slot_token[q0 + i];
+      s_tgt[i] = target_token[q0 + i];
+    }
+  }
+  __syncthreads();
+  auto par_of = [&](int x) { return staged ? s_par[x] : slot_parent[q0 + x]; };
+  auto tok_of = [&](int x) { return staged ? s_tok[x] : slot_token[q0 + x]; };
+  auto tgt_of = [&](int x) { return staged ? s_tgt[x] : target_token[q0 + x]; };
   int bits = 0;
   // best (depth, slot) of this lane; slot 0 (the root) is always valid at depth 0
   int best_d = 0, best_s = 0;
   for (int s = 1 + lane; s < n; s += kWave) {
-    const int own_p = slot_parent[q0 + s];
+    const int own_p = par_of(s);
     if (own_p < 0 || own_p >= s) bits |= ECHO_DATA_BAD_SLOT_PARENT;
     bool ok = true;
     int depth = 0;
     int x = s;
     while (x > 0) {
-      const int p = slot_parent[q0 + x];
+      const int p = par_of(x);
       if (p < 0 || p >= x) { ok = false; break; }
-      if (slot_token[q0 + x] != target_token[q0 + p]) { ok = false; break; }
+      if (tok_of(x) != tgt_of(p)) { ok = false; break; }
       ++depth;
       x = p;
     }
@@ -66,10 +85,10 @@ __global__ __launch_bounds__(kWave) void accept_kernel(
     int x = best_s;
     for (int i = best_d - 1; i >= 0; --i) {
       out_slots[i] = q0 + x;
-      x = slot_parent[q0 + x];
+      x = par_of(x);
     }
     accept_len[r] = best_d;
-    bonus_token[r] = target_token[q0 + best_s];
+    bonus_token[r] = tgt_of(best_s);
   }
 }
 

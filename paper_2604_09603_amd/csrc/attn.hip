@@ -29,6 +29,8 @@
 //                 workgroup.
 //   attn_combine  one thread per (cut unit, stream, row, 4 dims): merges the
 //                 partials in range order (deterministic) into out and lse.
+#include <hip/hip_ext.h>
+
 #include "echo_device.h"
 #include "echo_internal.h"
 
@@ -796,6 +798,7 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
 // kCombineBlocks workgroups.  The partials are merged in workgroup order.
 constexpr int kCombineItems = kWaves * kPassRows * (kD / 4);
 constexpr int kCombineBlocks = kCombineItems / kThreads;
+constexpr int kFastParts = 4;  // cuts over at most this many workgroups merge in one round trip
 static_assert(kCombineItems % kThreads == 0, "combine tiling");
 
 __global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv, int G, AttnWs ws,
@@ -814,6 +817,41 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv,
   const int nparts = c.b1 - c.b0 + 1;
   // partial of part i: workgroup b0 + i, whose segment may sit in its second slot
   auto prow_of = [&](int i) { return part_row(c.b0 + i, i == 0 ? c.first_slot : 0, w, rho); };
+  const int ra = sm.row0 + rho;
+  const size_t orow = size_t(u.q0 + ra / G) * hq + sm.kvh * G + ra % G;
+  if (nparts <= kFastParts) {
+    // every load issued at once: one memory round trip
+    float2 ml[kFastParts];
+    floatx4 po[kFastParts];
+#pragma unroll
+    for (int i = 0; i < kFastParts; ++i) {
+      ml[i] = make_float2(-__builtin_inff(), 0.0f);
+      po[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+      if (i < nparts) {
+        const size_t prow = prow_of(i);
+        ml[i] = *reinterpret_cast<const float2*>(ws.part_ml + prow * 2);
+        po[i] = *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
+      }
+    }
+    float M = -__builtin_inff();
+#pragma unroll
+    for (int i = 0; i < kFastParts; ++i) M = fmaxf(M, ml[i].x);
+    float L = 0.0f;
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    if (M != -__builtin_inff()) {
+#pragma unroll
+      for (int i = 0; i < kFastParts; ++i) {
+        if (ml[i].x == -__builtin_inff()) continue;  // absent or empty part
+        const float wgt = __builtin_amdgcn_exp2f(ml[i].x - M);
+        L += wgt * ml[i].y;
+        acc += wgt * po[i];
+      }
+    }
+    const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+    *reinterpret_cast<floatx4*>(out + orow * kD + d4) = acc * inv;
+    if (lse != nullptr && d4 == 0) lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
+    return;
+  }
   float M = -__builtin_inff();
   for (int i = 0; i < nparts; ++i) M = fmaxf(M, ws.part_ml[prow_of(i) * 2]);
   float L = 0.0f;
@@ -828,8 +866,6 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv,
       acc += wgt * *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
     }
   }
-  const int ra = sm.row0 + rho;
-  const size_t orow = size_t(u.q0 + ra / G) * hq + sm.kvh * G + ra % G;
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
   *reinterpret_cast<floatx4*>(out + orow * kD + d4) = acc * inv;
   if (lse != nullptr && d4 == 0) lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
@@ -866,11 +902,15 @@ int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
   m.scale2 = a.sm_scale * kLog2e;
   m.out = a.out;
   m.lse = a.lse;
+  // the measurement events (if set) travel in the dispatch packet itself: no
+  // extra packets, no cache flushes between the launches
   const bool prof = g_attn_ev_start != nullptr && g_attn_ev_stop != nullptr;
-  if (prof && hipEventRecord(g_attn_ev_start, stream) != hipSuccess) return ECHO_ERR_HIP;
-  hipLaunchKernelGGL(attn_main_kernel, dim3(unsigned(nb)), dim3(kWaves * kWave), 0, stream, m,
-                     ws);
-  if (prof && hipEventRecord(g_attn_ev_stop, stream) != hipSuccess) return ECHO_ERR_HIP;
+  void* main_args[] = {&m, &ws};
+  if (hipExtLaunchKernel(reinterpret_cast<const void*>(&attn_main_kernel), dim3(unsigned(nb)),
+                         dim3(kWaves * kWave), main_args, 0, stream,
+                         prof ? g_attn_ev_start : nullptr, prof ? g_attn_ev_stop : nullptr,
+                         0) != hipSuccess)
+    return ECHO_ERR_HIP;
   // cut units number fewer than the main kernel's workgroups
   hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(nb * kCombineBlocks)), dim3(kThreads), 0,
                      stream, a.hq, a.hkv, G, ws, a.out, a.lse);

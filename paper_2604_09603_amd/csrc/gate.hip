@@ -5,15 +5,18 @@
 //   gate_score   one thread per candidate: root->leaf binary32 fold of the path
 //                score, 32-bit orderable key, and each block's 2048-bin histogram
 //                of the key's top 11 bits, written to its own slice.
-//   gate_bin     one block: sums the block histograms and finds the bin b* that
-//                holds the m-th largest key, m = min(B, #finite), and how many
-//                keys of b* are selected.
+//   gate_bin     one block: from the blocks' finite counts and highest occupied
+//                bins, sums the block histograms downwards from the top in
+//                chunks of 64 bins until it finds the bin b* that holds the
+//                m-th largest key, m = min(B, #finite), and how many keys of b*
+//                are selected (usually one chunk: the selection is a small top).
 //   gate_select  one thread per candidate: keys above b* are selected, keys below
 //                are not; keys inside b* go to the block's own candidate slice.
-//   gate_finish  one block: gathers the candidates, sorts them in LDS by (key
-//                descending, index ascending), selects the head and checks the
-//                ancestor closure of the selection.  If b* holds more keys than
-//                the sort takes, it falls back to radix refinement over all keys.
+//   gate_finish  one block: gathers the candidates into LDS, finds the
+//                threshold (key descending, index ascending) among them by radix
+//                selection, selects the head and checks the ancestor closure of
+//                the selection.  If b* holds more keys than LDS takes, the same
+//                selection runs over all keys in place.
 #include "echo_device.h"
 #include "echo_internal.h"
 
@@ -23,8 +26,9 @@ namespace {
 constexpr int kGateThreads = 1024;
 constexpr int kHistBins = 2048;   // top 11 bits of the key
 constexpr int kHistShift = 21;
-constexpr int kSortCap = 4096;    // candidates gate_finish sorts in LDS
-constexpr int kGatherCap = 4096;  // keys the fallback holds in LDS
+constexpr int kSortCap = 8192;    // candidates gate_finish gathers into LDS
+constexpr int kWinBack = 3072;    // nodes before a score block kept in its LDS window
+constexpr int kWin = kWinBack + kGateThreads;
 
 struct GateMeta {
   int32_t num_selected;  // m
@@ -41,6 +45,7 @@ struct GateWs {
   int32_t* pglob;    // [N] clamped parent, global index (-1: child of the root)
   uint32_t* bhist;   // [nblocks][2048] per-block histograms
   uint32_t* ccount;  // [nblocks] candidates found by each select block
+  uint2* bsum;       // [nblocks] (finite keys, highest occupied bin + 1) of each score block
   uint2* cand;       // [nblocks * 1024] (key, index) candidates, block slices
 };
 
@@ -64,6 +69,8 @@ __host__ __device__ inline GateWs gate_ws_layout(void* base, int32_t N) {
   p += align_up(nb * kHistBins * 4, 256);
   w.ccount = reinterpret_cast<uint32_t*>(p);
   p += align_up(nb * 4, 256);
+  w.bsum = reinterpret_cast<uint2*>(p);
+  p += align_up(nb * 8, 256);
   w.cand = reinterpret_cast<uint2*>(p);
   return w;
 }
@@ -71,7 +78,7 @@ __host__ __device__ inline GateWs gate_ws_layout(void* base, int32_t N) {
 size_t gate_ws_bytes(int32_t N) {
   const size_t nb = size_t(gate_blocks(N));
   return 256 + 2 * align_up(size_t(N) * 4, 256) + align_up(nb * kHistBins * 4, 256) +
-         align_up(nb * 4, 256) + align_up(nb * kGateThreads * 8, 256);
+         align_up(nb * 4, 256) + align_up(nb * 8, 256) + align_up(nb * kGateThreads * 8, 256);
 }
 
 // ---------------------------------------------------------------- score ----
@@ -82,7 +89,18 @@ __global__ __launch_bounds__(kGateThreads) void gate_score_kernel(
   extern __shared__ int32_t s_offs[];  // R + 1 entries
   __shared__ uint32_t s_hist[kHistBins];
   __shared__ int s_flag;
+  // parent and log q of the block's nodes and of the kWinBack nodes before them:
+  // the ancestors of most nodes lie there, so the path walks stay in LDS
+  __shared__ int32_t s_par[kWin];
+  __shared__ float s_lq[kWin];
+  const int g0 = blockIdx.x * kGateThreads;
+  const int wstart = max(0, g0 - kWinBack);
+  const int wlen = min(N, g0 + kGateThreads) - wstart;
 
+  for (int i = threadIdx.x; i < wlen; i += kGateThreads) {
+    s_par[i] = parent[wstart + i];
+    s_lq[i] = logq[wstart + i];
+  }
   for (int i = threadIdx.x; i <= R; i += kGateThreads) s_offs[i] = cand_offsets[i];
   for (int i = threadIdx.x; i < kHistBins; i += kGateThreads) s_hist[i] = 0u;
   if (threadIdx.x == 0) s_flag = 0;
@@ -104,10 +122,12 @@ __global__ __launch_bounds__(kGateThreads) void gate_score_kernel(
       const int r = upper_bound_idx(s_offs, R + 1, g);
       const int lo = s_offs[r];
       const int n = g - lo;
-      int p = parent[g];
+      auto par_at = [&](int a) { return a >= wstart ? s_par[a - wstart] : parent[a]; };
+      auto lq_at = [&](int a) { return a >= wstart ? s_lq[a - wstart] : logq[a]; };
+      int p = par_at(g);
       if (p < -1 || p >= n) { bits |= ECHO_DATA_BAD_PARENT; p = -1; }
       pg = p < 0 ? -1 : lo + p;
-      float own = logq[g];
+      float own = lq_at(g);
       if (own != own) { bits |= ECHO_DATA_NAN_LOGQ; own = -__builtin_inff(); }
       else if (own > 0.0f) { bits |= ECHO_DATA_POS_LOGQ; own = 0.0f; }
       // collect log q along the path, leaf first: vals[0] = own, vals[i] = i-th ancestor
@@ -119,10 +139,10 @@ __global__ __launch_bounds__(kGateThreads) void gate_score_kernel(
         vals[i] = 0.0f;
         if (p >= 0) {
           const int a = lo + p;
-          float v = logq[a];
+          float v = lq_at(a);
           if (v != v) v = -__builtin_inff();
           else if (v > 0.0f) v = 0.0f;
-          int pp = parent[a];
+          int pp = par_at(a);
           if (pp < -1 || pp >= p) pp = -1;
           vals[i] = v;
           depth = i + 1;
@@ -149,44 +169,64 @@ __global__ __launch_bounds__(kGateThreads) void gate_score_kernel(
   wave_status_or(status, bits);
   __syncthreads();
   uint32_t* mine = ws.bhist + size_t(blockIdx.x) * kHistBins;
-  for (int i = threadIdx.x; i < kHistBins; i += kGateThreads) mine[i] = s_hist[i];
+  uint32_t fin = 0u, top = 0u;  // finite keys, highest occupied bin + 1
+  for (int i = threadIdx.x; i < kHistBins; i += kGateThreads) {
+    const uint32_t c = s_hist[i];
+    mine[i] = c;
+    fin += c;
+    if (c != 0u) top = max(top, uint32_t(i + 1));
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    fin += __shfl_xor(fin, off, kWave);
+    top = max(top, uint32_t(__shfl_xor(top, off, kWave)));
+  }
+  __shared__ uint2 s_red[kGateThreads / kWave];
+  if ((threadIdx.x & (kWave - 1)) == 0) s_red[threadIdx.x / kWave] = make_uint2(fin, top);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint2 acc = make_uint2(0u, 0u);
+    for (int w = 0; w < kGateThreads / kWave; ++w) {
+      acc.x += s_red[w].x;
+      acc.y = max(acc.y, s_red[w].y);
+    }
+    ws.bsum[blockIdx.x] = acc;
+  }
 }
 
 // ------------------------------------------------------------------ bin ----
+constexpr int kChunkBins = 64;                         // bins per downward step
+constexpr int kChunkGroups = kGateThreads / kChunkBins;  // blocks summed in parallel per bin
+
 __global__ __launch_bounds__(kGateThreads) void gate_bin_kernel(int nblocks, int budget, GateWs ws,
                                                                int32_t* __restrict__ num_selected) {
-  __shared__ int s_scan[kGateThreads / kWave + 1];
-  __shared__ uint32_t s_part[2][kHistBins];
-  constexpr int per = kHistBins / kGateThreads;  // bins per thread, high bins first
+  __shared__ uint32_t s_part[kChunkGroups][kChunkBins];
+  __shared__ uint2 s_red[kGateThreads / kWave];
+  __shared__ uint32_t s_state[3];  // running count above the chunk, found flag
   const int t = threadIdx.x;
-  {
-    // thread (half h, quad q) sums bins 4q..4q+3 over blocks h, h+2, ...; many loads in flight
-    const int h = t / (kGateThreads / 2);
-    const int q4 = (t % (kGateThreads / 2)) * 4;
-    uint4 acc = make_uint4(0, 0, 0, 0);
-#pragma unroll 8
-    for (int b = h; b < nblocks; b += 2) {
-      const uint4 v = *reinterpret_cast<const uint4*>(ws.bhist + size_t(b) * kHistBins + q4);
-      acc.x += v.x;
-      acc.y += v.y;
-      acc.z += v.z;
-      acc.w += v.w;
-    }
-    *reinterpret_cast<uint4*>(&s_part[h][q4]) = acc;
+  const int lane = t & (kWave - 1);
+  // 1. #finite keys and the highest occupied bin over all score blocks
+  uint32_t fin = 0u, top = 0u;
+  for (int b = t; b < nblocks; b += kGateThreads) {
+    const uint2 v = ws.bsum[b];
+    fin += v.x;
+    top = max(top, v.y);
   }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    fin += __shfl_xor(fin, off, kWave);
+    top = max(top, uint32_t(__shfl_xor(top, off, kWave)));
+  }
+  if (lane == 0) s_red[t / kWave] = make_uint2(fin, top);
   __syncthreads();
-  uint32_t cnt[per];
+  fin = 0u;
+  top = 0u;
 #pragma unroll
-  for (int j = 0; j < per; ++j) {
-    const int b = kHistBins - per * t - 1 - j;
-    cnt[j] = s_part[0][b] + s_part[1][b];
+  for (int w = 0; w < kGateThreads / kWave; ++w) {
+    fin += s_red[w].x;
+    top = max(top, s_red[w].y);
   }
-  uint32_t local = 0;
-#pragma unroll
-  for (int j = 0; j < per; ++j) local += cnt[j];
-  int finite;
-  const uint32_t above0 = uint32_t(block_exclusive_sum<kGateThreads>(int(local), s_scan, &finite));
-  const uint32_t m = min(uint32_t(budget), uint32_t(finite));
+  const uint32_t m = min(uint32_t(budget), fin);
   if (t == 0) {
     ws.meta->num_selected = int32_t(m);
     ws.meta->bin = 0u;
@@ -195,21 +235,47 @@ __global__ __launch_bounds__(kGateThreads) void gate_bin_kernel(int nblocks, int
     ws.meta->thr_key = 0xFFFFFFFFu;
     ws.meta->thr_g = -1;
     *num_selected = int32_t(m);
+    s_state[0] = 0u;  // keys in the bins above the current chunk
+    s_state[1] = 0u;  // found
   }
   __syncthreads();
   if (m == 0u) return;
-  uint32_t above = above0;
-  if (above < m && above + local >= m) {
-#pragma unroll
-    for (int j = 0; j < per; ++j) {
-      const int b = kHistBins - per * t - 1 - j;
-      if (above < m && above + cnt[j] >= m) {
-        ws.meta->bin = uint32_t(b);
-        ws.meta->bin_cnt = cnt[j];
-        ws.meta->bin_need = m - above;
-      }
-      above += cnt[j];
+  // 2. from the highest occupied bin downwards, 64 bins at a time
+  const int j = t % kChunkBins;   // bin offset below the chunk's top
+  const int grp = t / kChunkBins;  // blocks grp, grp + 16, ...
+  for (int hi = int(top) - 1; hi >= 0; hi -= kChunkBins) {
+    const int bin = hi - j;
+    uint32_t c = 0u;
+    if (bin >= 0) {
+#pragma unroll 4
+      for (int b = grp; b < nblocks; b += kChunkGroups) c += ws.bhist[size_t(b) * kHistBins + bin];
     }
+    s_part[grp][j] = c;
+    __syncthreads();
+    if (t < kWave) {  // one wave scans the chunk's 64 bins, highest first
+      uint32_t cnt = 0u;
+#pragma unroll
+      for (int g = 0; g < kChunkGroups; ++g) cnt += s_part[g][t];
+      uint32_t incl = cnt;  // inclusive sum over bins hi .. hi - t
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const uint32_t u = __shfl_up(incl, off, kWave);
+        if (t >= off) incl += u;
+      }
+      const uint32_t above = s_state[0];
+      const bool cross = above + incl >= m && above + incl - cnt < m;
+      if (cross) {
+        ws.meta->bin = uint32_t(hi - t);
+        ws.meta->bin_cnt = cnt;
+        ws.meta->bin_need = m - (above + incl - cnt);
+        s_state[1] = 1u;
+      }
+      const uint32_t total = __shfl(incl, kWave - 1, kWave);
+      if (t == 0) s_state[0] = above + total;
+    }
+    __syncthreads();
+    if (s_state[1] != 0u) break;
+    __syncthreads();  // s_part is rewritten by the next chunk
   }
 }
 
@@ -245,129 +311,131 @@ __global__ __launch_bounds__(kGateThreads) void gate_select_kernel(int N, GateWs
 }
 
 // --------------------------------------------------------------- finish ----
-// Fallback (the threshold bin holds more keys than the LDS sort takes): radix
-// refinement of the threshold key over all keys, ties by index in order.
-struct Refine {
-  uint32_t prefix;  // known high bits of the threshold key (value >> shift)
+// Radix selection: among the entries i < n with match(i), each carrying an
+// unsigned value val(i), find the value of the need-th largest, 8 bits at a
+// time from the top.  A step counts the entries whose value has the known high
+// bits into a 256-bin LDS histogram and one wave finds the bin where the count
+// from the top reaches need.  Once every entry matching the known bits is
+// selected (need == cnt) the lower bits no longer matter and the walk stops.
+struct RadixSel {
+  uint32_t prefix;  // known high bits of the value (value >> shift)
   int shift;        // number of still unknown low bits
-  uint32_t cnt;     // keys matching the known prefix
-  uint32_t need;    // how many of those are selected (1..cnt)
+  uint32_t need;    // rank of the sought entry among those matching the prefix (1..cnt)
+  uint32_t cnt;     // entries matching the prefix
 };
 
-template <typename Get>
-__device__ void refine_step(Refine& st, int n, Get get, uint32_t* s_h256, int* s_scan) {
-  const int bits = st.shift >= 8 ? 8 : st.shift;
-  const int nsh = st.shift - bits;
-  const uint32_t nb = 1u << bits;
-  for (int i = threadIdx.x; i < 256; i += blockDim.x) s_h256[i] = 0u;
-  __syncthreads();
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
-    const uint32_t k = get(i);
-    if (k != 0u && (k >> st.shift) == st.prefix) atomicAdd(&s_h256[(k >> nsh) & (nb - 1)], 1u);
+struct RadixLds {
+  uint32_t h[2][256];  // histograms, used alternately
+  int d[2][2];         // (bin, count above the bin) of each step
+};
+
+// One wave: the bin of h whose cumulative count from bin 255 downwards first
+// reaches need, and the count of the bins above it.
+__device__ __forceinline__ void digit_search(const uint32_t* h, uint32_t need, int* out) {
+  const int lane = threadIdx.x & (kWave - 1);
+  uint32_t c[4];
+  uint32_t sum = 0u;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {  // lane l holds bins 255-4l .. 252-4l, highest first
+    c[j] = h[255 - 4 * lane - j];
+    sum += c[j];
   }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t above = 0;
-    int d = int(nb) - 1;
-    for (; d > 0; --d) {
-      if (above + s_h256[d] >= st.need) break;
-      above += s_h256[d];
+  uint32_t incl = sum;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t u = __shfl_up(incl, off, kWave);
+    if (lane >= off) incl += u;
+  }
+  const unsigned long long hit = __ballot(incl >= need);
+  const int l0 = hit != 0ull ? __builtin_ctzll(hit) : 0;
+  if (lane == l0) {
+    uint32_t above = incl - sum;
+    int j = 0;
+    for (; j < 3; ++j) {
+      if (above + c[j] >= need) break;
+      above += c[j];
     }
-    s_scan[0] = d;
-    s_scan[1] = int(above);
+    out[0] = 255 - 4 * lane - j;
+    out[1] = int(above);
   }
-  __syncthreads();
-  const uint32_t d = uint32_t(s_scan[0]);
-  st.need -= uint32_t(s_scan[1]);
-  st.cnt = s_h256[d];
-  st.prefix = (st.prefix << bits) | d;
-  st.shift = nsh;
-  __syncthreads();
 }
 
-// Index of the `need`-th key equal to key_t in ascending order of i.
-template <typename Get, typename Idx>
-__device__ int32_t nth_equal(uint32_t key_t, uint32_t need, int n, Get get, Idx idx, int* s_scan,
-                             int* s_found) {
-  if (threadIdx.x == 0) *s_found = -1;
-  __syncthreads();
-  uint32_t run = 0;
-  for (int base = 0; base < n; base += blockDim.x) {
-    const int i = base + threadIdx.x;
-    const int f = (i < n && get(i) == key_t) ? 1 : 0;
-    int tot;
-    const int ex = block_exclusive_sum<kGateThreads>(f, s_scan, &tot);
-    if (f && run + uint32_t(ex) + 1u == need) *s_found = idx(i);
-    run += uint32_t(tot);
-    if (run >= need) break;  // uniform: run is the same in every thread
-  }
-  __syncthreads();
-  return *s_found;
-}
-
-__device__ void refine_threshold(const GateWs& ws, int N, uint32_t* thr_key, int32_t* thr_g,
-                                 uint32_t* s_gk, int32_t* s_gi) {
-  __shared__ uint32_t s_h256[256];
-  __shared__ int s_scan[kGateThreads / kWave + 1];
-  __shared__ int s_found;
-  Refine st;
-  st.prefix = ws.meta->bin;
-  st.shift = kHistShift;
-  st.cnt = ws.meta->bin_cnt;
-  st.need = ws.meta->bin_need;
-  const uint32_t* keys = ws.keys;
-  auto gget = [&](int i) { return keys[i]; };
-  while (st.shift > 0 && st.cnt > uint32_t(kGatherCap)) refine_step(st, N, gget, s_h256, s_scan);
-  int32_t tg;
-  if (st.cnt <= uint32_t(kGatherCap)) {
-    // ordered gather of the remaining keys (ascending candidate index) into LDS
-    const int sh = st.shift;
-    const uint32_t pre = st.prefix;
-    int filled = 0;
-    for (int base = 0; base < N; base += kGateThreads) {
-      const int g = base + threadIdx.x;
-      const uint32_t k = g < N ? keys[g] : 0u;
-      const int f = (k != 0u && (k >> sh) == pre) ? 1 : 0;
-      int tot;
-      const int ex = block_exclusive_sum<kGateThreads>(f, s_scan, &tot);
-      if (f) {
-        s_gk[filled + ex] = k;
-        s_gi[filled + ex] = g;
+// The histograms of both buffers must be zero on entry; they are on return.
+template <typename Val, typename Match>
+__device__ void radix_select(RadixSel& st, int n, Val val, Match match, RadixLds& L) {
+  int cur = 0;
+  while (st.shift > 0 && st.need < st.cnt) {
+    const int bits = st.shift >= 8 ? 8 : st.shift;
+    const int nsh = st.shift - bits;
+    const uint32_t pre = st.prefix, sh = uint32_t(st.shift);
+    for (int i = threadIdx.x; i < n; i += blockDim.x) {
+      if (match(i)) {
+        const uint32_t v = val(i);
+        if ((v >> sh) == pre) atomicAdd(&L.h[cur][(v >> nsh) & ((1u << bits) - 1u)], 1u);
       }
-      filled += tot;
-      if (uint32_t(filled) >= st.cnt) break;
     }
     __syncthreads();
-    auto lget = [&](int i) { return s_gk[i]; };
-    while (st.shift > 0) refine_step(st, filled, lget, s_h256, s_scan);
-    tg = st.need == st.cnt ? 0x7FFFFFFF
-                           : nth_equal(st.prefix, st.need, filled, lget,
-                                       [&](int i) { return s_gi[i]; }, s_scan, &s_found);
-  } else {
-    tg = st.need == st.cnt ? 0x7FFFFFFF
-                           : nth_equal(st.prefix, st.need, N, gget,
-                                       [](int i) { return int32_t(i); }, s_scan, &s_found);
+    if (threadIdx.x < kWave) {
+      digit_search(L.h[cur], st.need, L.d[cur]);
+    } else {  // the other buffer was read before the barrier above
+      for (int i = threadIdx.x - kWave; i < 256; i += blockDim.x - kWave) L.h[cur ^ 1][i] = 0u;
+    }
+    __syncthreads();
+    const int d = L.d[cur][0];
+    st.need -= uint32_t(L.d[cur][1]);
+    st.cnt = L.h[cur][d];
+    st.prefix = (pre << bits) | uint32_t(d);
+    st.shift = nsh;
+    cur ^= 1;
   }
-  *thr_key = st.prefix;
-  *thr_g = tg;
+  __syncthreads();  // every thread has read the last histogram
+  for (int i = threadIdx.x; i < 512; i += blockDim.x) (&L.h[0][0])[i] = 0u;
+  __syncthreads();
 }
 
-__device__ __forceinline__ uint64_t sort_word(uint32_t key, int32_t g) {
-  // larger key first, then smaller index first
-  return (uint64_t(key) << 32) | uint64_t(0xFFFFFFFFu - uint32_t(g));
+// Threshold (thr_key, thr_g) of the selection: the bin_need-th largest of the
+// bin_cnt keys of bin b* under (key descending, index ascending).  keyv(i) and
+// idx(i) describe the n entries searched; every key of b* must be among them.
+template <typename KeyV, typename Idx>
+__device__ void find_threshold(const GateMeta& mt, int n, int N, KeyV keyv, Idx idx, RadixLds& L,
+                               uint32_t* thr_key, int32_t* thr_g) {
+  RadixSel st;
+  st.prefix = mt.bin;
+  st.shift = kHistShift;
+  st.need = mt.bin_need;
+  st.cnt = mt.bin_cnt;
+  radix_select(st, n, keyv, [&](int i) { return keyv(i) != 0u; }, L);
+  const uint32_t K = st.prefix << st.shift;
+  int32_t tg = 0x7FFFFFFF;
+  if (st.need < st.cnt) {
+    // st.shift == 0: cnt keys equal K, the need-th smallest index among them
+    // is the need-th largest of (N - 1 - index)
+    const uint32_t top = uint32_t(N - 1);
+    RadixSel si;
+    si.prefix = 0u;
+    si.shift = top == 0u ? 0 : 32 - __builtin_clz(top);
+    si.need = st.need;
+    si.cnt = st.cnt;
+    radix_select(si, n, [&](int i) { return top - uint32_t(idx(i)); },
+                 [&](int i) { return keyv(i) == K; }, L);
+    tg = int32_t(top - (si.prefix << si.shift));
+  }
+  *thr_key = K;
+  *thr_g = tg;
 }
 
 __global__ __launch_bounds__(kGateThreads) void gate_finish_kernel(int N, int nblocks, GateWs ws,
                                                                    uint8_t* __restrict__ selected,
                                                                    int32_t* status) {
-  __shared__ uint64_t s_sort[kSortCap];  // also the fallback's gather buffers
+  __shared__ uint32_t s_k[kSortCap];  // gathered candidates: key
+  __shared__ int32_t s_g[kSortCap];   // and index
   __shared__ int s_base[kGateThreads + 1];
   __shared__ int s_scan[kGateThreads / kWave + 1];
-  __shared__ uint32_t s_tk;
-  __shared__ int32_t s_tg;
-  const uint32_t m = uint32_t(ws.meta->num_selected);
+  __shared__ RadixLds s_rl;
+  const GateMeta mt = *ws.meta;
+  const uint32_t m = uint32_t(mt.num_selected);
   if (m == 0u) return;
-  const uint32_t need = ws.meta->bin_need;
+  for (int i = threadIdx.x; i < 512; i += kGateThreads) (&s_rl.h[0][0])[i] = 0u;
   // exclusive scan of the per-block candidate counts
   int run = 0;
   for (int b0 = 0; b0 < nblocks; b0 += kGateThreads) {
@@ -379,86 +447,51 @@ __global__ __launch_bounds__(kGateThreads) void gate_finish_kernel(int N, int nb
     run += tot;
   }
   const int nc = run;
+  uint32_t tk;
+  int32_t tg;
   int bits = 0;
+  auto closed = [&](int32_t p) {  // is the parent p of a selected node selected?
+    if (p < 0) return true;
+    const uint32_t kp = ws.keys[p];
+    return kp != 0u && (kp > tk || (kp == tk && p <= tg));
+  };
   if (nc <= kSortCap && nblocks <= kGateThreads) {
     if (threadIdx.x == 0) s_base[nblocks] = nc;
     __syncthreads();
-    uint32_t n2 = 1;
-    while (n2 < uint32_t(nc)) n2 <<= 1;
-    for (uint32_t i = threadIdx.x; i < n2; i += kGateThreads) {
-      uint64_t w = 0ull;
-      if (i < uint32_t(nc)) {
-        const int b = upper_bound_idx(s_base, nblocks + 1, int(i));
-        const uint2 c = ws.cand[size_t(b) * kGateThreads + (int(i) - s_base[b])];
-        w = sort_word(c.x, int32_t(c.y));
-      }
-      s_sort[i] = w;
+    for (int i = threadIdx.x; i < nc; i += kGateThreads) {
+      const int b = upper_bound_idx(s_base, nblocks + 1, i);
+      const uint2 c = ws.cand[size_t(b) * kGateThreads + (i - s_base[b])];
+      s_k[i] = c.x;
+      s_g[i] = int32_t(c.y);
     }
     __syncthreads();
-    // bitonic sort, descending
-    for (uint32_t size = 2; size <= n2; size <<= 1) {
-      for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
-        for (uint32_t i = threadIdx.x; i < n2; i += kGateThreads) {
-          const uint32_t j = i ^ stride;
-          if (j > i) {
-            const uint64_t a = s_sort[i], b = s_sort[j];
-            const bool desc = (i & size) == 0;
-            if (desc ? (a < b) : (a > b)) {
-              s_sort[i] = b;
-              s_sort[j] = a;
-            }
-          }
-        }
-        __syncthreads();
-      }
-    }
-    const uint64_t thr = s_sort[need - 1];
-    if (threadIdx.x == 0) {
-      ws.meta->thr_key = uint32_t(thr >> 32);
-      ws.meta->thr_g = int32_t(0xFFFFFFFFu - uint32_t(thr));
-    }
-    for (uint32_t i = threadIdx.x; i < uint32_t(nc); i += kGateThreads) {
-      const uint64_t w = s_sort[i];
-      const int32_t gi = int32_t(0xFFFFFFFFu - uint32_t(w));
-      const bool sel = i < need;
-      selected[gi] = sel ? 1 : 0;
-      if (sel) {
-        const int32_t p = ws.pglob[gi];
-        if (p >= 0) {
-          const uint32_t kp = ws.keys[p];
-          if (kp == 0u || sort_word(kp, p) < thr) bits |= ECHO_DATA_NOT_CLOSED;
-        }
-      }
+    find_threshold(mt, nc, N, [&](int i) { return s_k[i]; }, [&](int i) { return s_g[i]; }, s_rl,
+                   &tk, &tg);
+    for (int i = threadIdx.x; i < nc; i += kGateThreads) {
+      const uint32_t k = s_k[i];
+      const int32_t g = s_g[i];
+      const bool sel = k > tk || (k == tk && g <= tg);
+      selected[g] = sel ? 1 : 0;
+      if (sel && !closed(ws.pglob[g])) bits |= ECHO_DATA_NOT_CLOSED;
     }
   } else {
-    uint32_t tk;
-    int32_t tg;
-    refine_threshold(ws, N, &tk, &tg, reinterpret_cast<uint32_t*>(s_sort),
-                     reinterpret_cast<int32_t*>(s_sort) + kGatherCap);
-    if (threadIdx.x == 0) {
-      s_tk = tk;
-      s_tg = tg;
-      ws.meta->thr_key = tk;
-      ws.meta->thr_g = tg;
-    }
     __syncthreads();
-    tk = s_tk;
-    tg = s_tg;
+    const uint32_t* keys = ws.keys;
+    find_threshold(mt, N, N, [&](int i) { return keys[i]; }, [](int i) { return int32_t(i); },
+                   s_rl, &tk, &tg);
     for (int b = 0; b < nblocks; ++b) {
       const int c = int(ws.ccount[b]);
       for (int i = threadIdx.x; i < c; i += kGateThreads) {
         const uint2 e = ws.cand[size_t(b) * kGateThreads + i];
         const bool sel = e.x > tk || (e.x == tk && int32_t(e.y) <= tg);
         selected[e.y] = sel ? 1 : 0;
-        if (sel) {
-          const int32_t p = ws.pglob[e.y];
-          if (p >= 0) {
-            const uint32_t kp = ws.keys[p];
-            if (kp == 0u || !(kp > tk || (kp == tk && p <= tg))) bits |= ECHO_DATA_NOT_CLOSED;
-          }
-        }
+        if (sel && !closed(ws.pglob[e.y])) bits |= ECHO_DATA_NOT_CLOSED;
       }
     }
+  }
+  if (threadIdx.x == 0) {
+    ws.meta->thr_key = tk;
+    ws.meta->thr_g = tg;
   }
   wave_status_or(status, bits);
 }

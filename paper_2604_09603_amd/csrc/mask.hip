@@ -4,11 +4,16 @@
 // One workgroup of 1024 threads (the selection holds at most B <= 16384 nodes,
 // so the whole step is latency-bound and a single CU avoids any grid-wide
 // synchronisation):
-//   1. ordered compaction of `selected` (64 bytes per thread per round, one
+//   1. ordered compaction of `selected` (128 bytes per thread per round, one
 //      block scan per round) into an LDS list of global indices, ascending;
-//   2. q_offsets[r] = r + #(packed candidates before request r) (binary search);
-//   3. one thread per slot walks its candidate's ancestor chain, marking the
-//      packed ancestors (binary search in the LDS list) in its bitmask row.
+//   2. q_offsets[r] = r + #(packed candidates before request r) (binary search)
+//      and the root slot of each request;
+//   3. one thread per packed node writes its slot's candidate and token and
+//      finds the local slot of its nearest packed ancestor (its parent, unless
+//      the selection is not ancestor-closed), kept in LDS: one round of global
+//      loads for all nodes;
+//   4. one thread per slot walks that chain in LDS only, marking its
+//      ancestors in its bitmask row.
 #include "echo_device.h"
 #include "echo_internal.h"
 
@@ -16,8 +21,9 @@ namespace echo {
 namespace {
 
 constexpr int kMaskThreads = 1024;
-constexpr int kBytesPerThread = 64;
+constexpr int kBytesPerThread = 128;
 constexpr int kRegWords = 8;  // mask words kept in registers; the rest is updated in memory
+constexpr int kRootsPerThread = (ECHO_MAX_REQUESTS + kMaskThreads) / kMaskThreads;
 
 // First index i in [lo, hi) with a[i] >= x (hi if none).
 __device__ __forceinline__ int lower_bound_lds(const int32_t* a, int lo, int hi, int32_t x) {
@@ -28,28 +34,47 @@ __device__ __forceinline__ int lower_bound_lds(const int32_t* a, int lo, int hi,
   return lo;
 }
 
+// Selection flags of 128 consecutive candidates as a 128-bit mask (bit b: byte
+// start + b is non-zero).
+struct Flags {
+  uint64_t lo, hi;
+};
+
+// Non-zero bytes of a 32-bit word as 4 bits (byte i -> bit i).
+__device__ __forceinline__ uint32_t nonzero_bytes(uint32_t w) {
+  uint32_t y = w | (w >> 4);
+  y |= y >> 2;
+  y |= y >> 1;
+  y &= 0x01010101u;                  // bit 0 of each byte: that byte was non-zero
+  return (y * 0x02040810u) >> 25 & 0xFu;  // gather bits 0, 8, 16, 24 at 25..28
+}
+
 template <bool kAligned>
-__device__ __forceinline__ uint64_t load_flags(const uint8_t* __restrict__ sel, int start, int N) {
-  uint64_t bits = 0;
+__device__ __forceinline__ Flags load_flags(const uint8_t* __restrict__ sel, int start, int N) {
+  Flags f = {0ull, 0ull};
   if (kAligned && start + kBytesPerThread <= N) {
     const uint4* p = reinterpret_cast<const uint4*>(sel + start);
+    uint4 w[8];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      uint4 w = p[v];
-      uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+    for (int v = 0; v < 8; ++v) w[v] = p[v];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int b = 0; b < 4; ++b)
-          if ((ws[u] >> (8 * b)) & 0xFFu) bits |= uint64_t(1) << (16 * v + 4 * u + b);
+    for (int v = 0; v < 8; ++v) {
+      const uint64_t nib = uint64_t(nonzero_bytes(w[v].x)) | (uint64_t(nonzero_bytes(w[v].y)) << 4) |
+                           (uint64_t(nonzero_bytes(w[v].z)) << 8) |
+                           (uint64_t(nonzero_bytes(w[v].w)) << 12);
+      if (v < 4) f.lo |= nib << (16 * v);
+      else f.hi |= nib << (16 * (v - 4));
     }
   } else {
     for (int b = 0; b < kBytesPerThread; ++b) {
-      int g = start + b;
-      if (g < N && sel[g] != 0) bits |= uint64_t(1) << b;
+      const int g = start + b;
+      if (g < N && sel[g] != 0) {
+        if (b < 64) f.lo |= uint64_t(1) << b;
+        else f.hi |= uint64_t(1) << (b - 64);
+      }
     }
   }
-  return bits;
+  return f;
 }
 
 template <bool kAligned>
@@ -64,12 +89,28 @@ __global__ __launch_bounds__(kMaskThreads) void mask_kernel(
   extern __shared__ int32_t smem[];
   int32_t* s_offs = smem;              // R + 1
   int32_t* s_qoff = smem + (R + 1);    // R + 1
-  int32_t* s_comp = smem + 2 * (R + 1);  // budget
+  int32_t* s_plen = smem + 2 * (R + 1);  // R + 1 (prefix lengths)
+  int32_t* s_comp = smem + 3 * (R + 1);  // budget
+  // local slot of each packed node's nearest packed ancestor (0: the root)
+  uint16_t* s_pslot = reinterpret_cast<uint16_t*>(smem + 3 * (R + 1) + budget);
   __shared__ int s_scan[kMaskThreads / kWave + 1];
   __shared__ int s_flag;
 
   const int tid = threadIdx.x;
-  for (int i = tid; i <= R; i += kMaskThreads) s_offs[i] = cand_offsets[i];
+  // the first round of flags is loaded together with the CSR
+  Flags f0 = tid * kBytesPerThread < N ? load_flags<kAligned>(selected, tid * kBytesPerThread, N)
+                                       : Flags{0ull, 0ull};
+  // root tokens of this thread's requests (r = tid + 1024 k), stored in step 2
+  int32_t rtok[kRootsPerThread];
+#pragma unroll
+  for (int k = 0; k < kRootsPerThread; ++k) {
+    const int r = tid + kMaskThreads * k;
+    rtok[k] = r < R ? root_token[r] : 0;
+  }
+  for (int i = tid; i <= R; i += kMaskThreads) {
+    s_offs[i] = cand_offsets[i];
+    if (i < R) s_plen[i] = prefix_len[i];
+  }
   __syncthreads();
   if (tid == 0) s_flag = (s_offs[0] != 0 || s_offs[R] != N) ? 1 : 0;
   __syncthreads();
@@ -85,14 +126,20 @@ __global__ __launch_bounds__(kMaskThreads) void mask_kernel(
   if (ok) {
     for (int base = 0; base < N; base += kMaskThreads * kBytesPerThread) {
       const int start = base + tid * kBytesPerThread;
-      uint64_t f = start < N ? load_flags<kAligned>(selected, start, N) : 0ull;
+      Flags f = base == 0 ? f0
+                          : (start < N ? load_flags<kAligned>(selected, start, N)
+                                       : Flags{0ull, 0ull});
       int tot;
-      int pos = count + block_exclusive_sum<kMaskThreads>(__popcll(f), s_scan, &tot);
-      while (f) {
-        int b = __ffsll(static_cast<long long>(f)) - 1;
-        f &= f - 1;
-        if (pos < budget) s_comp[pos] = start + b;
-        ++pos;
+      int pos = count + block_exclusive_sum<kMaskThreads>(__popcll(f.lo) + __popcll(f.hi), s_scan,
+                                                          &tot);
+      for (int half = 0; half < 2; ++half) {
+        uint64_t m = half ? f.hi : f.lo;
+        while (m) {
+          const int b = __ffsll(static_cast<long long>(m)) - 1;
+          m &= m - 1;
+          if (pos < budget) s_comp[pos] = start + 64 * half + b;
+          ++pos;
+        }
       }
       count += tot;
     }
@@ -101,11 +148,18 @@ __global__ __launch_bounds__(kMaskThreads) void mask_kernel(
   const int n_inc = count < budget ? count : budget;
   __syncthreads();
 
-  // 2. slot offsets
-  for (int r = tid; r < R; r += kMaskThreads) {
+  // 2. slot offsets and the root slots
+#pragma unroll
+  for (int k = 0; k < kRootsPerThread; ++k) {
+    const int r = tid + kMaskThreads * k;
+    if (r >= R) break;
     int v = r + lower_bound_lds(s_comp, 0, n_inc, s_offs[r]);
     s_qoff[r] = v;
     q_offsets[r] = v;
+    slot_cand[v] = -1;
+    slot_parent[v] = -1;
+    slot_token[v] = rtok[k];
+    position_ids[v] = s_plen[r];
   }
   if (tid == 0) {
     s_qoff[R] = R + n_inc;
@@ -113,7 +167,35 @@ __global__ __launch_bounds__(kMaskThreads) void mask_kernel(
   }
   __syncthreads();
 
-  // 3. one thread per slot
+  // 3. nearest packed ancestor of every packed node, as a local slot
+  for (int i = tid; i < n_inc; i += kMaskThreads) {
+    const int g = s_comp[i];
+    const int r = upper_bound_idx(s_offs, R + 1, g);  // request of g
+    const int lo = s_offs[r];
+    const int cbase = s_qoff[r] - r;                  // list index of the request's first packed node
+    const int cend = s_qoff[r + 1] - (r + 1);
+    int p = parent[g];
+    const int s = s_qoff[r] + 1 + (i - cbase);  // this node's slot
+    slot_cand[s] = g;
+    slot_token[s] = token[g];
+    if (p < -1 || p >= g - lo) { bits |= ECHO_DATA_BAD_PARENT; p = -1; }
+    int pslot = 0;
+    bool first = true;
+    while (p >= 0) {
+      const int x = lo + p;
+      const int idx = lower_bound_lds(s_comp, cbase, cend, x);
+      if (idx < cend && s_comp[idx] == x) { pslot = idx - cbase + 1; break; }
+      if (first) bits |= ECHO_DATA_NOT_CLOSED;  // attach to the nearest packed ancestor
+      first = false;
+      int pp = parent[x];
+      if (pp < -1 || pp >= p) { bits |= ECHO_DATA_BAD_PARENT; pp = -1; }
+      p = pp;
+    }
+    s_pslot[i] = static_cast<uint16_t>(pslot);
+  }
+  __syncthreads();
+
+  // 4. one thread per slot: ancestor bits, parent slot, depth
   const int nslots = R + n_inc;
   for (int s = tid; s < nslots; s += kMaskThreads) {
     const int r = upper_bound_idx(s_qoff, R + 1, s);
@@ -124,16 +206,8 @@ __global__ __launch_bounds__(kMaskThreads) void mask_kernel(
     for (int w = 0; w < kRegWords; ++w) regs[w] = 0u;
     for (int w = kRegWords; w < W; ++w) row[w] = 0u;
     regs[0] = 1u;  // the root is everyone's ancestor
-    if (j == 0) {
-      slot_cand[s] = -1;
-      slot_parent[s] = -1;
-      slot_token[s] = root_token[r];
-      position_ids[s] = prefix_len[r];
-    } else {
-      const int cbase = s_qoff[r] - r;             // list index of the request's first packed node
-      const int cend = s_qoff[r + 1] - (r + 1);
-      const int g = s_comp[s - r - 1];
-      const int lo = s_offs[r];
+    if (j > 0) {
+      const int cbase = s_qoff[r] - r;
       auto set_bit = [&](int lj) {
         const int w = lj >> 5;
         const uint32_t m = 1u << (lj & 31);
@@ -146,31 +220,16 @@ __global__ __launch_bounds__(kMaskThreads) void mask_kernel(
         }
       };
       set_bit(j);
-      int p = parent[g];
-      if (p < -1 || p >= g - lo) { bits |= ECHO_DATA_BAD_PARENT; p = -1; }
-      int pj = 0;
+      const int pj = s_pslot[cbase + j - 1];
       int depth = 1;
-      bool found_parent = false;
-      while (p >= 0) {
-        const int x = lo + p;
-        const int idx = lower_bound_lds(s_comp, cbase, cend, x);
-        if (idx < cend && s_comp[idx] == x) {
-          const int lj = idx - cbase + 1;
-          if (!found_parent) { pj = lj; found_parent = true; }
-          set_bit(lj);
-          ++depth;
-        } else if (!found_parent) {
-          bits |= ECHO_DATA_NOT_CLOSED;
-        }
-        int pp = parent[x];
-        if (pp < -1 || pp >= p) { bits |= ECHO_DATA_BAD_PARENT; pp = -1; }
-        p = pp;
+      // local slots strictly decrease along the chain, so the walk ends
+      for (int x = pj; x > 0; x = s_pslot[cbase + x - 1]) {
+        set_bit(x);
+        ++depth;
       }
       if (depth > ECHO_MAX_DEPTH) bits |= ECHO_DATA_TOO_DEEP;
-      slot_cand[s] = g;
       slot_parent[s] = pj;
-      slot_token[s] = token[g];
-      position_ids[s] = prefix_len[r] + depth;
+      position_ids[s] = s_plen[r] + depth;
     }
 #pragma unroll
     for (int w = 0; w < kRegWords; ++w)
@@ -182,7 +241,7 @@ __global__ __launch_bounds__(kMaskThreads) void mask_kernel(
 }  // namespace
 
 size_t mask_lds_bytes(int32_t R, int32_t budget) {
-  return size_t(2 * (R + 1) + budget) * sizeof(int32_t);
+  return size_t(3 * (R + 1) + budget) * sizeof(int32_t) + size_t(budget) * sizeof(uint16_t);
 }
 
 int32_t launch_build_tree_mask(const int32_t* cand_offsets, const int32_t* parent,

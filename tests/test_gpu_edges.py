@@ -138,6 +138,23 @@ def test_all_equal_scores_large_tie_class():
         _check_all(b, attention=(budget == 241))
 
 
+def test_crowded_threshold_bin():
+    """20k distinct path scores inside one 11-bit key bin: the threshold is found
+    over more keys than the finish kernel gathers into LDS, and at budgets whose
+    boundary falls inside the bin."""
+    rng = np.random.default_rng(11)
+    R, n = 4, 5000
+    offs = np.arange(R + 1, dtype=np.int32) * n
+    parent = np.full(R * n, -1, np.int32)
+    logq = rng.uniform(-0.99, -0.88, R * n).astype(np.float32)
+    pool = dict(cand_offsets=offs, parent=parent, token=np.zeros(R * n, np.int32),
+                logq=logq, root_token=np.zeros(R, np.int32))
+    for budget in (1, 700, 4097, 12345):
+        print(f"[edges] crowded bin B={budget}", flush=True)
+        b = make_micro_batch(pool, budget, hq=4, hkv=2, p_range=(10, 20))
+        _check_all(b, attention=False)
+
+
 def test_empty_requests_and_prefixes():
     offs = np.array([0, 0, 4, 4, 7], np.int32)            # requests 0 and 2 have no candidates
     parent = np.array([-1, 0, 0, 1, -1, -1, 1], np.int32)
