@@ -10,7 +10,9 @@ Stages (each module cites the passage it follows):
 
 * ``gate``   -- path scores (eq. 5) and the budgeted global selection under the
                batch-level verification cap (eq. 4; budget-exchange argument of
-               Theorem 2 and Proposition 1).
+               Theorem 2 and Proposition 1); ``gate_sparse`` first truncates
+               each request at its first failed checkpoint depth (layer
+               confidence eq. 6, gating signal eq. 7, Alg. 1 phase 1).
 * ``mask``   -- flatten & pack of the selected super-tree into per-request
                verify slots, position ids and ancestor bitmasks (Fig. 3, stage 3).
 * ``attn``   -- tree-masked grouped-query attention of every verify slot over
@@ -24,7 +26,7 @@ word (bit values in ``status``) and the offending value is clamped as each
 function documents.
 """
 from . import status
-from .gate import path_scores, select_top_b, gate
+from .gate import path_scores, select_top_b, gate, gate_sparse
 from .mask import build_tree_mask
 from .attn import tree_verify_attn
 from .accept import accept

@@ -116,3 +116,88 @@ def gate(cand_offsets, parent, logq, budget):
                 status |= st.NOT_CLOSED
     return dict(path_score=S, depth=depth, selected=sel,
                 num_selected=int(sel.sum()), status=status)
+
+
+# ---------------------------------------------------------------------------
+# Sparse gating at checkpoint depths (Section 3.2, eq. 6 and eq. 7; Alg. 1).
+#
+# Layer confidence (eq. 6): c_{i,d} = exp(max over request i's depth-d nodes
+# of S).  Gating signal (eq. 7): g_{i,d} = [c_{i,d} > tau_d], evaluated only
+# at the calibrated checkpoint depths d in D_sig.  The comparison is taken in
+# the log domain, max S > ln tau_d, with ln tau_d supplied by the caller as a
+# float32 (exp is monotone, so this is the same test without an exp).
+#
+# Reading of the truncation (Alg. 1, phase 1): the scheduler walks the depths
+# in order and a request whose checkpoint test fails at depth d leaves the
+# active set before its depth-d tokens are appended, so none of its nodes at
+# depth >= d is verified.  The freed budget returns to the shared pool, which
+# the global top-B of eq. 4 then spends on the remaining nodes (other
+# requests' depth, or this request's width above d).  Depths that are not
+# checkpoints always pass.
+# ---------------------------------------------------------------------------
+
+def layer_max_scores(cand_offsets, S, depth):
+    """max S per (request, depth): array [R, MAX_DEPTH + 1] of float32, -inf
+    where a request has no node (or only -inf nodes) at that depth.  Column 0
+    (the root) is unused.  This is eq. 6 before the exp."""
+    offs = np.asarray(cand_offsets, np.int64)
+    R = len(offs) - 1
+    out = np.full((R, st.MAX_DEPTH + 1), -np.inf, np.float32)
+    if not csr_ok(offs, len(S)):
+        return out
+    for r in range(R):
+        for g in range(int(offs[r]), int(offs[r + 1])):
+            d = int(depth[g])
+            if 1 <= d <= st.MAX_DEPTH and S[g] > out[r, d]:
+                out[r, d] = S[g]
+    return out
+
+
+def truncation_depths(layer_max, sig_depth, log_tau):
+    """First failing checkpoint per request (eq. 7), MAX_DEPTH + 1 if none fails.
+
+    Checkpoint k sits at depth sig_depth[k] with threshold ln tau = log_tau[k];
+    request i fails it iff NOT (layer_max[i, d] > log_tau[k]) in float32.
+    """
+    R = layer_max.shape[0]
+    t = np.full(R, st.MAX_DEPTH + 1, np.int32)
+    for i in range(R):
+        for d, lt in zip(sig_depth, log_tau):
+            d = int(d)
+            passed = bool(np.float32(layer_max[i, d]) > np.float32(lt))
+            if not passed and d < t[i]:
+                t[i] = d
+    return t
+
+
+def gate_sparse(cand_offsets, parent, logq, budget, sig_depth, log_tau):
+    """Sparse-gated selection: the checkpoint truncation of eq. 7, then the
+    global top-B of eq. 4 over the nodes that survive it.
+
+    Returns the dict of ``gate`` plus ``trunc_depth`` [R] (first failing
+    checkpoint, MAX_DEPTH + 1 if none) and ``layer_max`` [R, MAX_DEPTH + 1].
+    ``path_score`` is the untruncated eq. 5 score.
+    """
+    S, depth, status = path_scores(cand_offsets, parent, logq)
+    offs = np.asarray(cand_offsets, np.int64)
+    R = len(offs) - 1
+    lm = layer_max_scores(offs, S, depth)
+    t = truncation_depths(lm, sig_depth, log_tau)
+    S_gate = S.copy()
+    if csr_ok(offs, len(S)):
+        for r in range(R):
+            for g in range(int(offs[r]), int(offs[r + 1])):
+                if depth[g] >= t[r]:
+                    S_gate[g] = -np.inf
+    sel = select_top_b(S_gate, budget)
+    if not csr_ok(offs, len(S)):
+        return dict(path_score=S, depth=depth, selected=sel, num_selected=0, status=status,
+                    trunc_depth=t, layer_max=lm)
+    par = clamped_parents(offs, parent)
+    for r in range(R):
+        lo, hi = int(offs[r]), int(offs[r + 1])
+        for g in range(lo, hi):
+            if sel[g] and par[g] >= 0 and not sel[lo + par[g]]:
+                status |= st.NOT_CLOSED
+    return dict(path_score=S, depth=depth, selected=sel, num_selected=int(sel.sum()),
+                status=status, trunc_depth=t, layer_max=lm)
