@@ -66,6 +66,7 @@ typedef void* echo_stream_t; /* hipStream_t */
 #define ECHO_HEAD_DIM 128       /* the only supported head dimension                 */
 #define ECHO_MAX_BUDGET 16384   /* largest budget B                                  */
 #define ECHO_MAX_REQUESTS 4095  /* largest batch R                                   */
+#define ECHO_MAX_CHECKPOINTS 16 /* entries of a sparse-gating checkpoint table       */
 
 /*
  * echo_gate -- path scores and the global top-B selection.
@@ -96,6 +97,43 @@ int32_t echo_gate(const int32_t* cand_offsets, const int32_t* parent, const floa
                   int32_t* num_selected, void* workspace, size_t workspace_bytes, int32_t* status,
                   echo_stream_t stream);
 size_t echo_gate_workspace_size(int32_t R, int32_t N, int32_t budget);
+
+/*
+ * echo_gate_sparse -- echo_gate preceded by sparse gating at checkpoint depths
+ * (Section 3.2: layer confidence eq. 6, gating signal eq. 7; truncation as in
+ * phase 1 of Alg. 1).
+ *
+ * For every request r and checkpoint depth d the layer confidence is the
+ * largest path score among r's depth-d candidates (eq. 6 without the exp;
+ * -inf if there is none).  Request r passes the checkpoint iff that maximum is
+ * strictly greater than ln tau_d (eq. 7 in the log domain, compared in
+ * binary32).  At the first checkpoint depth t_r it fails, the request is
+ * truncated: none of its candidates at depth >= t_r can be selected.  The
+ * global top-B of echo_gate then runs over the candidates that remain, so the
+ * budget a truncated request frees goes to the other requests' depth or to
+ * this request's width above t_r.
+ *
+ *   sig_depth    [num_sig] int32  HOST array: checkpoint depths, 1..ECHO_MAX_DEPTH
+ *                                 (1 = the root's children); a depth listed twice
+ *                                 must pass both thresholds
+ *   log_tau      [num_sig] float  HOST array: ln tau of each checkpoint; -inf
+ *                                 passes any depth with a finite score, +inf or
+ *                                 0 passes none (scores are <= 0); NaN is refused
+ *   num_sig                       0..ECHO_MAX_CHECKPOINTS (0: no truncation)
+ *   trunc_depth  [R]       int32  (nullable) t_r, ECHO_MAX_DEPTH + 1 if none fails
+ * The checkpoint table is read on the host during the call and travels in the
+ * kernel arguments (a captured graph keeps the values of capture time).  All
+ * other arguments, outputs, clamps and status bits are those of echo_gate;
+ * path_score holds the untruncated eq. 5 scores.  The workspace is that of
+ * echo_gate (echo_gate_sparse_workspace_size returns the same size).
+ */
+int32_t echo_gate_sparse(const int32_t* cand_offsets, const int32_t* parent, const float* logq,
+                         int32_t R, int32_t N, int32_t budget, const int32_t* sig_depth,
+                         const float* log_tau, int32_t num_sig, float* path_score,
+                         uint8_t* selected, int32_t* num_selected, int32_t* trunc_depth,
+                         void* workspace, size_t workspace_bytes, int32_t* status,
+                         echo_stream_t stream);
+size_t echo_gate_sparse_workspace_size(int32_t R, int32_t N, int32_t budget);
 
 /*
  * echo_build_tree_mask -- flatten & pack the selection into verify slots

@@ -7,9 +7,13 @@
 
 namespace echo {
 
+// num_sig == 0: plain top-B; otherwise sparse checkpoint gating first (host
+// arrays sig_depth / log_tau of num_sig entries, already validated).
 int32_t launch_gate(const int32_t* cand_offsets, const int32_t* parent, const float* logq,
-                    int32_t R, int32_t N, int32_t budget, float* path_score, uint8_t* selected,
-                    int32_t* num_selected, void* workspace, int32_t* status, hipStream_t stream);
+                    int32_t R, int32_t N, int32_t budget, const int32_t* sig_depth,
+                    const float* log_tau, int32_t num_sig, float* path_score, uint8_t* selected,
+                    int32_t* num_selected, int32_t* trunc_depth, void* workspace, int32_t* status,
+                    hipStream_t stream);
 size_t gate_workspace_bytes(int32_t R, int32_t N, int32_t budget);
 
 int32_t launch_build_tree_mask(const int32_t* cand_offsets, const int32_t* parent,

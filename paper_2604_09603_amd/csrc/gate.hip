@@ -17,6 +17,13 @@
 //                selection, selects the head and checks the ancestor closure of
 //                the selection.  If b* holds more keys than LDS takes, the same
 //                selection runs over all keys in place.
+//
+// Sparse checkpoint gating (eq. 6, eq. 7; Alg. 1 phase 1) adds two launches in
+// front of gate_bin: gate_lmax_clear zeroes the per-(request, depth) maximum
+// keys, gate_score then also folds each block's checkpoint-depth keys into
+// them (LDS first, one global atomicMax per block, request and depth) instead
+// of building histograms, and gate_trunc finds each request's first failed
+// checkpoint, zeroes the keys at or below it and builds the histograms.
 #include "echo_device.h"
 #include "echo_internal.h"
 
@@ -29,6 +36,8 @@ constexpr int kHistShift = 21;
 constexpr int kSortCap = 8192;    // candidates gate_finish gathers into LDS
 constexpr int kWinBack = 3072;    // nodes before a score block kept in its LDS window
 constexpr int kWin = kWinBack + kGateThreads;
+constexpr int kDepths = ECHO_MAX_DEPTH + 1;  // per-request depth slots (0 = root, unused)
+constexpr int kTabReq = 64;                  // requests per score block with an LDS max table
 
 struct GateMeta {
   int32_t num_selected;  // m
@@ -47,6 +56,17 @@ struct GateWs {
   uint32_t* ccount;  // [nblocks] candidates found by each select block
   uint2* bsum;       // [nblocks] (finite keys, highest occupied bin + 1) of each score block
   uint2* cand;       // [nblocks * 1024] (key, index) candidates, block slices
+  uint32_t* lmax;    // [R][kDepths] max key per (request, depth), checkpoint depths only
+  uint8_t* depth;    // [N] node depth (1 = child of the root), capped at ECHO_MAX_DEPTH + 1
+};
+
+// Checkpoint table of sparse gating: request r passes depth d iff the largest
+// path score among its depth-d nodes is above lt[d] (eq. 7 in the log domain).
+struct SparseArgs {
+  int enabled;
+  uint32_t mask;     // bit d set iff depth d is a checkpoint
+  float lt[kDepths]; // ln tau of each checkpoint depth (the largest if repeated)
+  int32_t* trunc_out;  // nullable [R]: first failed checkpoint, ECHO_MAX_DEPTH + 1 if none
 };
 
 __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -55,7 +75,7 @@ __host__ __device__ inline int gate_blocks(int32_t N) {
   return N > 0 ? (N + kGateThreads - 1) / kGateThreads : 1;
 }
 
-__host__ __device__ inline GateWs gate_ws_layout(void* base, int32_t N) {
+__host__ __device__ inline GateWs gate_ws_layout(void* base, int32_t N, int32_t R) {
   const size_t nb = size_t(gate_blocks(N));
   char* p = static_cast<char*>(base);
   GateWs w;
@@ -72,23 +92,58 @@ __host__ __device__ inline GateWs gate_ws_layout(void* base, int32_t N) {
   w.bsum = reinterpret_cast<uint2*>(p);
   p += align_up(nb * 8, 256);
   w.cand = reinterpret_cast<uint2*>(p);
+  p += align_up(nb * kGateThreads * 8, 256);
+  w.lmax = reinterpret_cast<uint32_t*>(p);
+  p += align_up(size_t(R) * kDepths * 4, 256);
+  w.depth = reinterpret_cast<uint8_t*>(p);
   return w;
 }
 
-size_t gate_ws_bytes(int32_t N) {
+size_t gate_ws_bytes(int32_t N, int32_t R) {
   const size_t nb = size_t(gate_blocks(N));
   return 256 + 2 * align_up(size_t(N) * 4, 256) + align_up(nb * kHistBins * 4, 256) +
-         align_up(nb * 4, 256) + align_up(nb * 8, 256) + align_up(nb * kGateThreads * 8, 256);
+         align_up(nb * 4, 256) + align_up(nb * 8, 256) + align_up(nb * kGateThreads * 8, 256) +
+         align_up(size_t(R) * kDepths * 4, 256) + align_up(size_t(N), 256);
+}
+
+// Per-block histogram outputs shared by gate_score and gate_trunc: the block's
+// 2048 bins and (finite keys, highest occupied bin + 1).
+__device__ void write_block_hist(const uint32_t* s_hist, uint2* s_red, GateWs& ws) {
+  uint32_t* mine = ws.bhist + size_t(blockIdx.x) * kHistBins;
+  uint32_t fin = 0u, top = 0u;
+  for (int i = threadIdx.x; i < kHistBins; i += kGateThreads) {
+    const uint32_t c = s_hist[i];
+    mine[i] = c;
+    fin += c;
+    if (c != 0u) top = max(top, uint32_t(i + 1));
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    fin += __shfl_xor(fin, off, kWave);
+    top = max(top, uint32_t(__shfl_xor(top, off, kWave)));
+  }
+  if ((threadIdx.x & (kWave - 1)) == 0) s_red[threadIdx.x / kWave] = make_uint2(fin, top);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint2 acc = make_uint2(0u, 0u);
+    for (int w = 0; w < kGateThreads / kWave; ++w) {
+      acc.x += s_red[w].x;
+      acc.y = max(acc.y, s_red[w].y);
+    }
+    ws.bsum[blockIdx.x] = acc;
+  }
 }
 
 // ---------------------------------------------------------------- score ----
 __global__ __launch_bounds__(kGateThreads) void gate_score_kernel(
     const int32_t* __restrict__ cand_offsets, const int32_t* __restrict__ parent,
     const float* __restrict__ logq, int R, int N, GateWs ws, float* __restrict__ path_score_out,
-    int32_t* status) {
+    int32_t* status, SparseArgs sp) {
   extern __shared__ int32_t s_offs[];  // R + 1 entries
   __shared__ uint32_t s_hist[kHistBins];
+  __shared__ uint32_t s_lmax[kTabReq * kDepths];  // sparse gating: requests r0 .. r0 + 63
   __shared__ int s_flag;
+  __shared__ int s_r0;
   // parent and log q of the block's nodes and of the kWinBack nodes before them:
   // the ancestors of most nodes lie there, so the path walks stay in LDS
   __shared__ int32_t s_par[kWin];
@@ -103,6 +158,8 @@ __global__ __launch_bounds__(kGateThreads) void gate_score_kernel(
   }
   for (int i = threadIdx.x; i <= R; i += kGateThreads) s_offs[i] = cand_offsets[i];
   for (int i = threadIdx.x; i < kHistBins; i += kGateThreads) s_hist[i] = 0u;
+  if (sp.enabled)
+    for (int i = threadIdx.x; i < kTabReq * kDepths; i += kGateThreads) s_lmax[i] = 0u;
   if (threadIdx.x == 0) s_flag = 0;
   __syncthreads();
   // the candidate CSR must be well formed before anything is read through it
@@ -111,6 +168,8 @@ __global__ __launch_bounds__(kGateThreads) void gate_score_kernel(
     if (s_offs[r + 1] < s_offs[r]) s_flag = 1;
   __syncthreads();
   const bool ok = s_flag == 0;
+  if (sp.enabled && threadIdx.x == 0) s_r0 = ok && g0 < N ? upper_bound_idx(s_offs, R + 1, g0) : 0;
+  if (sp.enabled) __syncthreads();
 
   const int g = blockIdx.x * kGateThreads + threadIdx.x;
   int bits = 0;
@@ -159,7 +218,15 @@ __global__ __launch_bounds__(kGateThreads) void gate_score_kernel(
           if (i < depth) s = s + vals[i];
       }
       key = score_key(s);
-      if (key != 0u) atomicAdd(&s_hist[key >> kHistShift], 1u);
+      if (!sp.enabled) {
+        if (key != 0u) atomicAdd(&s_hist[key >> kHistShift], 1u);
+      } else if (key != 0u && ((sp.mask >> depth) & 1u)) {
+        // depth <= ECHO_MAX_DEPTH here: deeper nodes have key 0
+        const int rl = r - s_r0;
+        if (rl < kTabReq) atomicMax(&s_lmax[rl * kDepths + depth], key);
+        else atomicMax(&ws.lmax[size_t(r) * kDepths + depth], key);
+      }
+      if (sp.enabled) ws.depth[g] = uint8_t(min(depth, ECHO_MAX_DEPTH + 1));
     }
     ws.keys[g] = key;
     ws.pglob[g] = pg;
@@ -168,30 +235,86 @@ __global__ __launch_bounds__(kGateThreads) void gate_score_kernel(
   if (!ok && blockIdx.x == 0 && threadIdx.x == 0) bits |= ECHO_DATA_BAD_OFFSETS;
   wave_status_or(status, bits);
   __syncthreads();
-  uint32_t* mine = ws.bhist + size_t(blockIdx.x) * kHistBins;
-  uint32_t fin = 0u, top = 0u;  // finite keys, highest occupied bin + 1
-  for (int i = threadIdx.x; i < kHistBins; i += kGateThreads) {
-    const uint32_t c = s_hist[i];
-    mine[i] = c;
-    fin += c;
-    if (c != 0u) top = max(top, uint32_t(i + 1));
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    fin += __shfl_xor(fin, off, kWave);
-    top = max(top, uint32_t(__shfl_xor(top, off, kWave)));
-  }
   __shared__ uint2 s_red[kGateThreads / kWave];
-  if ((threadIdx.x & (kWave - 1)) == 0) s_red[threadIdx.x / kWave] = make_uint2(fin, top);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint2 acc = make_uint2(0u, 0u);
-    for (int w = 0; w < kGateThreads / kWave; ++w) {
-      acc.x += s_red[w].x;
-      acc.y = max(acc.y, s_red[w].y);
+  if (!sp.enabled) {
+    write_block_hist(s_hist, s_red, ws);
+  } else {
+    // one global atomic per (request, checkpoint depth) present in the block
+    for (int i = threadIdx.x; i < kTabReq * kDepths; i += kGateThreads) {
+      const uint32_t v = s_lmax[i];
+      const int r = s_r0 + i / kDepths;
+      if (v != 0u && r < R) atomicMax(&ws.lmax[size_t(r) * kDepths + i % kDepths], v);
     }
-    ws.bsum[blockIdx.x] = acc;
   }
+}
+
+// --------------------------------------------------------- sparse gating ----
+__global__ __launch_bounds__(kGateThreads) void gate_lmax_clear_kernel(int n, uint32_t* lmax) {
+  const int i = blockIdx.x * kGateThreads + threadIdx.x;
+  if (i < n) lmax[i] = 0u;
+}
+
+// First failed checkpoint of request r: the smallest checkpoint depth d whose
+// maximum key does not exceed the key of ln tau_d (eq. 7; -0 == +0 and -inf
+// has key 0 on both sides, so the key test is the float test S > ln tau).
+__device__ __forceinline__ int first_failed(const SparseArgs& sp, const uint32_t* lmax_r) {
+  for (int d = 1; d <= ECHO_MAX_DEPTH; ++d)
+    if (((sp.mask >> d) & 1u) && !(lmax_r[d] > score_key(sp.lt[d]))) return d;
+  return ECHO_MAX_DEPTH + 1;
+}
+
+// One thread per candidate: keys at or below the request's truncation depth
+// become 0 (never selected); the block histogram is built from what is left.
+__global__ __launch_bounds__(kGateThreads) void gate_trunc_kernel(const int32_t* __restrict__ cand_offsets,
+                                                                 int R, int N, GateWs ws,
+                                                                 SparseArgs sp) {
+  extern __shared__ int32_t s_offs[];  // R + 1 entries
+  __shared__ uint32_t s_hist[kHistBins];
+  __shared__ uint8_t s_t[kGateThreads + 1];  // truncation depth of requests r0 .. r0 + 1024
+  __shared__ uint2 s_red[kGateThreads / kWave];
+  __shared__ int s_flag;
+  const int g0 = blockIdx.x * kGateThreads;
+  for (int i = threadIdx.x; i <= R; i += kGateThreads) s_offs[i] = cand_offsets[i];
+  for (int i = threadIdx.x; i < kHistBins; i += kGateThreads) s_hist[i] = 0u;
+  if (threadIdx.x == 0) s_flag = 0;
+  __syncthreads();
+  if (threadIdx.x == 0 && (s_offs[0] != 0 || s_offs[R] != N)) s_flag = 1;
+  for (int r = threadIdx.x; r < R; r += kGateThreads)
+    if (s_offs[r + 1] < s_offs[r]) s_flag = 1;
+  __syncthreads();
+  const bool ok = s_flag == 0;
+  // the requests of this block's candidates are r0 .. r1 (at most 1025 of them)
+  const int r0 = ok && g0 < N ? upper_bound_idx(s_offs, R + 1, g0) : 0;
+  const int r1 = ok && g0 < N ? upper_bound_idx(s_offs, R + 1, min(N, g0 + kGateThreads) - 1) : -1;
+  // (r1 - r0 exceeds 1024 only with empty requests in between: those beyond the
+  // table are looked up directly)
+  for (int r = r0 + int(threadIdx.x); r <= min(r1, r0 + kGateThreads); r += kGateThreads)
+    s_t[r - r0] = uint8_t(first_failed(sp, ws.lmax + size_t(r) * kDepths));
+  // the optional per-request output, spread over the blocks
+  if (sp.trunc_out != nullptr) {
+    const int per = (R + int(gridDim.x) - 1) / int(gridDim.x);
+    for (int r = blockIdx.x * per + threadIdx.x; r < min(R, (blockIdx.x + 1) * per);
+         r += kGateThreads)
+      sp.trunc_out[r] = ok ? first_failed(sp, ws.lmax + size_t(r) * kDepths) : ECHO_MAX_DEPTH + 1;
+  }
+  __syncthreads();
+  const int g = g0 + threadIdx.x;
+  if (ok && g < N) {
+    uint32_t key = ws.keys[g];
+    if (key != 0u) {
+      const int r = upper_bound_idx(s_offs, R + 1, g);
+      const int t = r - r0 <= kGateThreads ? int(s_t[r - r0])
+                                           : first_failed(sp, ws.lmax + size_t(r) * kDepths);
+      if (int(ws.depth[g]) >= t) {
+        key = 0u;
+        ws.keys[g] = 0u;
+      } else {
+        atomicAdd(&s_hist[key >> kHistShift], 1u);
+      }
+    }
+  }
+  __syncthreads();
+  write_block_hist(s_hist, s_red, ws);
 }
 
 // ------------------------------------------------------------------ bin ----
@@ -499,14 +622,35 @@ __global__ __launch_bounds__(kGateThreads) void gate_finish_kernel(int N, int nb
 }  // namespace
 
 int32_t launch_gate(const int32_t* cand_offsets, const int32_t* parent, const float* logq,
-                    int32_t R, int32_t N, int32_t budget, float* path_score, uint8_t* selected,
-                    int32_t* num_selected, void* workspace, int32_t* status, hipStream_t stream) {
+                    int32_t R, int32_t N, int32_t budget, const int32_t* sig_depth,
+                    const float* log_tau, int32_t num_sig, float* path_score, uint8_t* selected,
+                    int32_t* num_selected, int32_t* trunc_depth, void* workspace, int32_t* status,
+                    hipStream_t stream) {
   (void)hipGetLastError();  // clear errors left by unrelated runtime calls
-  GateWs ws = gate_ws_layout(workspace, N);
+  GateWs ws = gate_ws_layout(workspace, N, R);
   const int blocks = gate_blocks(N);
   const size_t lds = size_t(R + 1) * sizeof(int32_t);
+  SparseArgs sp{};
+  sp.enabled = num_sig > 0 || trunc_depth != nullptr ? 1 : 0;
+  sp.mask = 0u;
+  for (int d = 0; d < kDepths; ++d) sp.lt[d] = -__builtin_inff();
+  for (int k = 0; k < num_sig; ++k) {
+    const int d = sig_depth[k];
+    // a depth listed twice must pass both thresholds: keep the larger
+    if (!((sp.mask >> d) & 1u) || log_tau[k] > sp.lt[d]) sp.lt[d] = log_tau[k];
+    sp.mask |= 1u << d;
+  }
+  sp.trunc_out = trunc_depth;
+  if (sp.enabled) {
+    const int n = R * kDepths;
+    hipLaunchKernelGGL(gate_lmax_clear_kernel, dim3((n + kGateThreads - 1) / kGateThreads),
+                       dim3(kGateThreads), 0, stream, n, ws.lmax);
+  }
   hipLaunchKernelGGL(gate_score_kernel, dim3(blocks), dim3(kGateThreads), lds, stream,
-                     cand_offsets, parent, logq, R, N, ws, path_score, status);
+                     cand_offsets, parent, logq, R, N, ws, path_score, status, sp);
+  if (sp.enabled)
+    hipLaunchKernelGGL(gate_trunc_kernel, dim3(blocks), dim3(kGateThreads), lds, stream,
+                       cand_offsets, R, N, ws, sp);
   hipLaunchKernelGGL(gate_bin_kernel, dim3(1), dim3(kGateThreads), 0, stream, blocks, budget, ws,
                      num_selected);
   if (N > 0) {
@@ -519,9 +663,8 @@ int32_t launch_gate(const int32_t* cand_offsets, const int32_t* parent, const fl
 }
 
 size_t gate_workspace_bytes(int32_t R, int32_t N, int32_t budget) {
-  (void)R;
   (void)budget;
-  return gate_ws_bytes(N);
+  return gate_ws_bytes(N, R);
 }
 
 }  // namespace echo

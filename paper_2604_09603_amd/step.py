@@ -10,7 +10,8 @@ import numpy as np
 import torch
 
 from . import (HEAD_DIM, MAX_DEPTH, echo_accept, echo_build_tree_mask, echo_gate,
-               echo_tree_verify_attn, gate_workspace_size, tree_verify_attn_workspace_size)
+               echo_gate_sparse, echo_tree_verify_attn, gate_workspace_size,
+               tree_verify_attn_workspace_size)
 
 
 def _aligned_workspace(nbytes, device):
@@ -27,8 +28,13 @@ def _dev(a, device, dtype=None):
 
 
 class VerifyStep:
-    def __init__(self, batch, device="cuda:0", max_depth=MAX_DEPTH):
+    """``checkpoints``: optional sequence of (depth, ln tau) pairs; when given the
+    gate stage is echo_gate_sparse (checkpoint truncation, then top-B)."""
+
+    def __init__(self, batch, device="cuda:0", max_depth=MAX_DEPTH, checkpoints=None):
         cfg = batch["cfg"]
+        self.checkpoints = None if checkpoints is None else [(int(d), float(t))
+                                                             for d, t in checkpoints]
         self.cfg = cfg
         self.device = device
         self.R = cfg.R
@@ -60,6 +66,7 @@ class VerifyStep:
         self.path_score = torch.zeros(max(self.N, 1), dtype=torch.float32, device=d)
         self.selected = torch.zeros(max(self.N, 1), dtype=torch.uint8, device=d)
         self.num_selected = z32(1)
+        self.trunc_depth = z32(self.R)
         self.q_offsets = z32(self.R + 1)
         self.slot_cand = z32(self.cap)
         self.slot_parent = z32(self.cap)
@@ -79,9 +86,15 @@ class VerifyStep:
 
     # ---- the four stages -------------------------------------------------
     def gate(self, stream=None):
-        echo_gate(self.cand_offsets, self.parent, self.logq, self.R, self.N, self.B,
-                  self.path_score, self.selected, self.num_selected, self.gate_ws,
-                  status=self.status, stream=stream)
+        if self.checkpoints is None:
+            echo_gate(self.cand_offsets, self.parent, self.logq, self.R, self.N, self.B,
+                      self.path_score, self.selected, self.num_selected, self.gate_ws,
+                      status=self.status, stream=stream)
+        else:
+            echo_gate_sparse(self.cand_offsets, self.parent, self.logq, self.R, self.N, self.B,
+                             [d for d, _ in self.checkpoints], [t for _, t in self.checkpoints],
+                             self.path_score, self.selected, self.num_selected, self.gate_ws,
+                             trunc_depth=self.trunc_depth, status=self.status, stream=stream)
 
     def mask(self, stream=None):
         echo_build_tree_mask(self.cand_offsets, self.parent, self.token, self.selected,
@@ -119,7 +132,8 @@ class VerifyStep:
         nq = int(self.q_offsets[-1].item())
         return dict(
             path_score=g(self.path_score)[:self.N], selected=g(self.selected)[:self.N],
-            num_selected=int(self.num_selected.item()), q_offsets=g(self.q_offsets),
+            num_selected=int(self.num_selected.item()), trunc_depth=g(self.trunc_depth),
+            q_offsets=g(self.q_offsets),
             slot_cand=g(self.slot_cand), slot_parent=g(self.slot_parent),
             slot_token=g(self.slot_token), position_ids=g(self.position_ids),
             tree_mask=g(self.tree_mask).view(np.uint32), out=g(self.out), lse=g(self.lse),

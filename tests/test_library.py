@@ -41,6 +41,20 @@ def test_host_side_errors_need_no_gpu():
     assert lib.echo_gate(None, None, None, 0, 0, 0, None, None, None, None, 0, None, None) == pkg.ERR_INVALID_ARG
     assert lib.echo_gate(P(8), P(8), P(8), 1, 1, -1, None, P(8), P(8), P(256), 1 << 20, None, None) == pkg.ERR_INVALID_ARG
     assert lib.echo_gate(P(256), P(256), P(256), 1, 1, 4, None, P(256), P(256), P(256), 0, None, None) == pkg.ERR_WORKSPACE
+    # sparse gating: checkpoint depth outside 1..16, NaN ln tau, too many checkpoints
+    I = lambda *v: ctypes.cast((ctypes.c_int32 * len(v))(*v), P)
+    F = lambda *v: ctypes.cast((ctypes.c_float * len(v))(*v), P)
+    ws = lib.echo_gate_sparse_workspace_size(1, 1, 4)
+    assert ws == lib.echo_gate_workspace_size(1, 1, 4)
+    sparse = lambda d, t, n: lib.echo_gate_sparse(P(256), P(256), P(256), 1, 1, 4, d, t, n, None,
+                                                  P(256), P(256), None, P(256), ws, None, None)
+    assert sparse(I(0), F(-1.0), 1) == pkg.ERR_INVALID_ARG
+    assert sparse(I(17), F(-1.0), 1) == pkg.ERR_INVALID_ARG
+    assert sparse(I(2), F(float("nan")), 1) == pkg.ERR_INVALID_ARG
+    assert sparse(I(*range(1, 18)), F(*([-1.0] * 17)), 17) == pkg.ERR_INVALID_ARG
+    assert sparse(None, None, 1) == pkg.ERR_INVALID_ARG
+    assert lib.echo_gate_sparse(P(256), P(256), P(256), 1, 1, 4, I(2), F(-1.0), 1, None, P(256),
+                                P(256), None, P(256), ws - 1, None, None) == pkg.ERR_WORKSPACE
     assert lib.echo_tree_verify_attn_workspace_size(4, 20, 8, 8, 64) == 0
     assert lib.echo_tree_verify_attn(P(16), P(16), P(16), P(16), P(16), P(16), 10, P(16), P(16), 1,
                                      1, 4, 6, 4, 128, 1.0, P(16), None, P(256), 1 << 30, None,
