@@ -24,6 +24,31 @@ PEAK_BF16_TFLOPS = 2500.0
 METRIC = "verified tree nodes/sec (gate+verify-attn+accept), % HBM / MFMA peak"
 
 
+# Checkpoint tables for the gate policies other than plain top-B.  ln tau at
+# depth d is a + b (d - 1), (a, b) placed near the median per-request layer
+# maximum of each synthetic workload, so that about half of the requests stop
+# at each checkpoint.
+TAU_LINE = {"tiny": (-1.1, -0.55), "l8b": (-3.1, -2.5), "l70b": (-2.9, -2.6),
+            "q235b": (-3.0, -2.65), "long": (-2.1, -1.6)}
+
+
+def gate_checkpoints(policy, cfg_name, depth):
+    """(depth, ln tau) pairs of a gate policy: 'sparse' = checkpoints at depths
+    1, 3, 5 (the paper's sweet-spot form), 'dense' = every drafted depth,
+    'fixed' = every drafted depth at one threshold; 'topb' = none."""
+    if policy == "topb":
+        return None
+    a, b = TAU_LINE[cfg_name]
+    lt = lambda d: a + b * (d - 1)
+    if policy == "sparse":
+        return [(d, lt(d)) for d in (1, 3, 5) if d <= depth]
+    if policy == "dense":
+        return [(d, lt(d)) for d in range(1, depth + 1)]
+    if policy == "fixed":
+        return [(d, lt(3)) for d in range(1, depth + 1)]
+    raise ValueError(policy)
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -59,7 +84,7 @@ def traffic_from_profile(attn_src_hash):
     return d.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(batch, cfg, budget_s=12.0):
+def cpu_baseline(batch, cfg, checkpoints=None, budget_s=12.0):
     """The oracle as written, single-threaded, on a bounded sample of the workload."""
     import numpy as np
     from threadpoolctl import threadpool_limits
@@ -68,7 +93,12 @@ def cpu_baseline(batch, cfg, budget_s=12.0):
     import synth
     with threadpool_limits(limits=1):
         t0 = time.perf_counter()
-        g = oracle.gate(batch["cand_offsets"], batch["parent"], batch["logq"], cfg.budget)
+        if checkpoints is None:
+            g = oracle.gate(batch["cand_offsets"], batch["parent"], batch["logq"], cfg.budget)
+        else:
+            g = oracle.gate_sparse(batch["cand_offsets"], batch["parent"], batch["logq"],
+                                   cfg.budget, [d for d, _ in checkpoints],
+                                   np.array([t for _, t in checkpoints], np.float32))
         m = oracle.build_tree_mask(batch["cand_offsets"], batch["parent"], batch["token"],
                                    g["selected"], batch["root_token"], batch["prefix_len"],
                                    cfg.budget, cfg.mask_words)
@@ -111,6 +141,8 @@ def main():
     ap.add_argument("--config", default="q235b")
     ap.add_argument("--seed", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--gate-policy", default="topb", choices=["topb", "sparse", "dense", "fixed"],
+                    help="gate stage: global top-B (default) or checkpoint gating before it")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES, five times (the "
                          "reference kernel that scales the HBM byte counters)")
@@ -143,7 +175,8 @@ def main():
     t0 = time.time()
     batch = synth.make_batch(args.config, args.seed)
     log(f"generated in {time.time() - t0:.1f} s; uploading")
-    st = VerifyStep(batch, device="cuda:0")
+    checkpoints = gate_checkpoints(args.gate_policy, args.config, cfg.depth)
+    st = VerifyStep(batch, device="cuda:0", checkpoints=checkpoints)
     # the target model's argmax per slot is a stand-in input: gather it once for this batch
     st.gate()
     st.mask()
@@ -210,7 +243,8 @@ def main():
             "batch": cfg.R, "budget": cfg.budget, "verified_slots": nq,
             "draft_nodes": int(res["num_selected"]), "candidates": int(batch["cand_offsets"][-1]),
             "kv_prefix_tokens": int(batch["kv_offsets"][-1]), "seed": args.seed,
-            "parallelism": "single GPU",
+            "parallelism": "single GPU", "gate_policy": args.gate_policy,
+            "checkpoints": checkpoints,
         },
         "roofline": {
             "kernel": "attn_main_kernel",
@@ -230,7 +264,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = cpu_baseline(batch, cfg)
+        out["cpu_baseline"] = cpu_baseline(batch, cfg, checkpoints)
     print(json.dumps(out), flush=True)
 
 

@@ -155,3 +155,18 @@ def test_full_step_with_sparse_gate():
     gc.compare_front(res, dict(gate=g, mask=m, accept=a), int(b["cand_offsets"][-1]))
     assert np.array_equal(res["trunc_depth"], g["trunc_depth"])
     gc.compare_attn(res["out"], res["lse"], ro, rl, range(m["num_slots"]))
+
+
+@pytest.mark.parametrize("name", ["l8b", "q235b", "long"])
+def test_ablation_dense_and_fixed_threshold(name):
+    """The paper's ablation policies as checkpoint tables: dense gating (a
+    checkpoint at every depth, thresholds at the median layer maximum) and a
+    single fixed threshold at every depth."""
+    b = synth.make_batch(name, 1, attention=False)
+    depths = list(range(1, b["cfg"].depth + 1))
+    dense = _median_table(b, depths)
+    _log(f"[sparse] {name} dense gating {dense}")
+    check(b["cand_offsets"], b["parent"], b["logq"], b["cfg"].budget, depths, dense)
+    fixed = [dense[len(dense) // 2]] * len(depths)
+    _log(f"[sparse] {name} fixed threshold {fixed[0]}")
+    check(b["cand_offsets"], b["parent"], b["logq"], b["cfg"].budget, depths, fixed)

@@ -139,3 +139,17 @@ def test_layer_confidence_is_the_depth_maximum():
                     and S[g] is not None]
             want = max(vals) if vals else -np.inf
             assert float(res["layer_max"][r, d]) == want, (r, d)
+
+
+def test_fixed_threshold_on_a_chain_stops_where_the_score_crosses():
+    """Fixed tau at every depth on single chains: S falls along the chain, so
+    the first failed depth is the first node at or below ln tau."""
+    logq = np.array([-0.25, -0.5, -0.25, -1.0, -0.5], np.float32)
+    # S = -0.25, -0.75, -1.0, -2.0, -2.5
+    offs = np.array([0, 5], np.int32)
+    parent = np.array([-1, 0, 1, 2, 3], np.int32)
+    for lt, t in [(-0.1, 1), (-0.5, 2), (-1.0, 3), (-1.5, 4), (-2.25, 5), (-3.0, 6)]:  # depth 6 is empty: fails
+        res = oracle.gate_sparse(offs, parent, logq, 5, list(range(1, 17)),
+                                 np.full(16, lt, np.float32))
+        assert res["trunc_depth"].tolist() == [t], lt
+        assert res["selected"].tolist() == [1 if d < t else 0 for d in range(1, 6)]
