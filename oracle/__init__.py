@@ -13,6 +13,9 @@ Stages (each module cites the passage it follows):
                Theorem 2 and Proposition 1); ``gate_sparse`` first truncates
                each request at its first failed checkpoint depth (layer
                confidence eq. 6, gating signal eq. 7, Alg. 1 phase 1).
+* ``elastic``-- Alg. 1's elastic budget scheduler (phase 1 depth extension
+               with checkpoint gating, phase 2 width expansion) as a selection
+               policy over the drafted pool.
 * ``mask``   -- flatten & pack of the selected super-tree into per-request
                verify slots, position ids and ancestor bitmasks (Fig. 3, stage 3).
 * ``attn``   -- tree-masked grouped-query attention of every verify slot over
@@ -27,6 +30,7 @@ function documents.
 """
 from . import status
 from .gate import path_scores, select_top_b, gate, gate_sparse
+from .elastic import elastic_schedule
 from .mask import build_tree_mask
 from .attn import tree_verify_attn
 from .accept import accept
