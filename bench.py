@@ -84,7 +84,7 @@ def traffic_from_profile(attn_src_hash):
     return d.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(batch, cfg, checkpoints=None, budget_s=12.0):
+def cpu_baseline(batch, cfg, checkpoints=None, elastic=None, budget_s=12.0):
     """The oracle as written, single-threaded, on a bounded sample of the workload."""
     import numpy as np
     from threadpoolctl import threadpool_limits
@@ -93,7 +93,12 @@ def cpu_baseline(batch, cfg, checkpoints=None, budget_s=12.0):
     import synth
     with threadpool_limits(limits=1):
         t0 = time.perf_counter()
-        if checkpoints is None:
+        if elastic is not None:
+            g = oracle.elastic_schedule(batch["cand_offsets"], batch["parent"], batch["logq"],
+                                        cfg.budget, [d for d, _ in checkpoints],
+                                        np.array([t for _, t in checkpoints], np.float32),
+                                        elastic[0], elastic[1])
+        elif checkpoints is None:
             g = oracle.gate(batch["cand_offsets"], batch["parent"], batch["logq"], cfg.budget)
         else:
             g = oracle.gate_sparse(batch["cand_offsets"], batch["parent"], batch["logq"],
@@ -141,8 +146,11 @@ def main():
     ap.add_argument("--config", default="q235b")
     ap.add_argument("--seed", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--gate-policy", default="topb", choices=["topb", "sparse", "dense", "fixed"],
-                    help="gate stage: global top-B (default) or checkpoint gating before it")
+    ap.add_argument("--gate-policy", default="topb",
+                    choices=["topb", "sparse", "dense", "fixed", "elastic"],
+                    help="gate stage: global top-B (default), checkpoint gating before it, or "
+                         "Alg. 1's elastic scheduler (checkpoints at depths 1, 3, 5, W_topk = 2, "
+                         "W_max = the drafted branching)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES, five times (the "
                          "reference kernel that scales the HBM byte counters)")
@@ -175,8 +183,13 @@ def main():
     t0 = time.time()
     batch = synth.make_batch(args.config, args.seed)
     log(f"generated in {time.time() - t0:.1f} s; uploading")
-    checkpoints = gate_checkpoints(args.gate_policy, args.config, cfg.depth)
-    st = VerifyStep(batch, device="cuda:0", checkpoints=checkpoints)
+    elastic = None
+    if args.gate_policy == "elastic":
+        checkpoints = gate_checkpoints("sparse", args.config, cfg.depth)
+        elastic = (2, cfg.branch)
+    else:
+        checkpoints = gate_checkpoints(args.gate_policy, args.config, cfg.depth)
+    st = VerifyStep(batch, device="cuda:0", checkpoints=checkpoints, elastic=elastic)
     # the target model's argmax per slot is a stand-in input: gather it once for this batch
     st.gate()
     st.mask()
@@ -244,7 +257,7 @@ def main():
             "draft_nodes": int(res["num_selected"]), "candidates": int(batch["cand_offsets"][-1]),
             "kv_prefix_tokens": int(batch["kv_offsets"][-1]), "seed": args.seed,
             "parallelism": "single GPU", "gate_policy": args.gate_policy,
-            "checkpoints": checkpoints,
+            "checkpoints": checkpoints, "elastic_widths": elastic,
         },
         "roofline": {
             "kernel": "attn_main_kernel",
@@ -264,7 +277,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = cpu_baseline(batch, cfg, checkpoints)
+        out["cpu_baseline"] = cpu_baseline(batch, cfg, checkpoints, elastic)
     print(json.dumps(out), flush=True)
 
 

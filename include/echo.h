@@ -136,6 +136,46 @@ int32_t echo_gate_sparse(const int32_t* cand_offsets, const int32_t* parent, con
 size_t echo_gate_sparse_workspace_size(int32_t R, int32_t N, int32_t budget);
 
 /*
+ * echo_gate_elastic -- the selection made by the unified elastic budget
+ * scheduler of Alg. 1 (Section 3.3), applied to the drafted candidate pool.
+ *
+ * Phase 1 (global depth extension, priority 1) walks the depths d = 1, 2, ...
+ * while budget is left and some request is active; at each depth the active
+ * requests are served in request order.  A request's appendable depth-d
+ * candidates are those with a finite path score whose parent it already holds
+ * (the root at depth 1).  At a checkpoint depth it passes iff the largest
+ * appendable path score is strictly above ln tau_d (eq. 6 and eq. 7 in the log
+ * domain; no appendable candidate fails); other depths always pass.  A request
+ * that passes takes its min(w_topk, budget left, #appendable) best appendable
+ * candidates (path score descending, index ascending) and is charged that
+ * many; with none appendable it leaves the active set (its drafted tree is
+ * exhausted).  A request that fails is truncated at d and leaves the active
+ * set.  Phase 2 (opportunistic width expansion, priority 2) serves the
+ * truncated requests in request order while budget is left: a request
+ * truncated at depth t >= 2 adds its next best appendable depth-(t-1)
+ * candidates, min(budget left, w_max - its width there, #remaining), and is
+ * charged that many.  The selection is ancestor-closed by construction.
+ *
+ *   sig_depth, log_tau, num_sig   HOST checkpoint table, as for echo_gate_sparse
+ *   w_topk                        default width per depth, >= 1
+ *   w_max                         width a truncated request may widen to, >= 0
+ *   num_selected [1]    int32     number of selected candidates (<= budget)
+ *   trunc_depth  [R]    int32     (nullable) depth at which the request was
+ *                                 truncated in phase 1, ECHO_MAX_DEPTH + 1 if it
+ *                                 never was (including requests the budget ran
+ *                                 out before testing)
+ * Other arguments, clamps and status bits are those of echo_gate.  The
+ * workspace is larger than echo_gate's: echo_gate_elastic_workspace_size.
+ */
+int32_t echo_gate_elastic(const int32_t* cand_offsets, const int32_t* parent, const float* logq,
+                          int32_t R, int32_t N, int32_t budget, const int32_t* sig_depth,
+                          const float* log_tau, int32_t num_sig, int32_t w_topk, int32_t w_max,
+                          float* path_score, uint8_t* selected, int32_t* num_selected,
+                          int32_t* trunc_depth, void* workspace, size_t workspace_bytes,
+                          int32_t* status, echo_stream_t stream);
+size_t echo_gate_elastic_workspace_size(int32_t R, int32_t N, int32_t budget);
+
+/*
  * echo_build_tree_mask -- flatten & pack the selection into verify slots
  * (Fig. 3, stage 3; the paper gives no layout, this is the library's).
  *

@@ -33,6 +33,7 @@ HEAD_DIM = 128
 
 EXPORTS = [
     "echo_gate", "echo_gate_workspace_size", "echo_gate_sparse", "echo_gate_sparse_workspace_size",
+    "echo_gate_elastic", "echo_gate_elastic_workspace_size",
     "echo_build_tree_mask", "echo_build_tree_mask_workspace_size",
     "echo_tree_verify_attn", "echo_tree_verify_attn_workspace_size",
     "echo_accept", "echo_set_attn_profile_events", "echo_status_string", "echo_version",
@@ -52,6 +53,9 @@ _SIGS = {
     "echo_gate_sparse": (_I32, [_P, _P, _P, _I32, _I32, _I32, _P, _P, _I32, _P, _P, _P, _P, _P,
                                 _SZ, _P, _P]),
     "echo_gate_sparse_workspace_size": (_SZ, [_I32, _I32, _I32]),
+    "echo_gate_elastic": (_I32, [_P, _P, _P, _I32, _I32, _I32, _P, _P, _I32, _I32, _I32, _P, _P,
+                                 _P, _P, _P, _SZ, _P, _P]),
+    "echo_gate_elastic_workspace_size": (_SZ, [_I32, _I32, _I32]),
     "echo_build_tree_mask": (_I32, [_P, _P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P,
                                     _I32, _P, _SZ, _P, _P]),
     "echo_build_tree_mask_workspace_size": (_SZ, [_I32, _I32, _I32]),
@@ -164,6 +168,31 @@ def echo_gate_sparse(cand_offsets, parent, logq, R, N, budget, sig_depth, log_ta
                                    _stream(stream))
     if check:
         _check(code, "echo_gate_sparse")
+    return code
+
+
+def gate_elastic_workspace_size(R, N, budget) -> int:
+    return int(load().echo_gate_elastic_workspace_size(R, N, budget))
+
+
+def echo_gate_elastic(cand_offsets, parent, logq, R, N, budget, sig_depth, log_tau, w_topk, w_max,
+                      path_score, selected, num_selected, workspace, trunc_depth=None,
+                      status=None, stream=None, check=True):
+    """Alg. 1's elastic budget scheduler as a selection.  ``sig_depth`` and
+    ``log_tau`` are host sequences; the rest are device tensors."""
+    n = len(sig_depth)
+    if len(log_tau) != n:
+        raise ValueError("sig_depth and log_tau differ in length")
+    depths = (ctypes.c_int32 * max(n, 1))(*[int(x) for x in sig_depth])
+    taus = (ctypes.c_float * max(n, 1))(*[float(x) for x in log_tau])
+    code = load().echo_gate_elastic(_ptr(cand_offsets), _ptr(parent), _ptr(logq), R, N, budget,
+                                    ctypes.cast(depths, _P), ctypes.cast(taus, _P), n, w_topk,
+                                    w_max, _ptr(path_score), _ptr(selected), _ptr(num_selected),
+                                    _ptr(trunc_depth), _ptr(workspace),
+                                    workspace.numel() * workspace.element_size(), _ptr(status),
+                                    _stream(stream))
+    if check:
+        _check(code, "echo_gate_elastic")
     return code
 
 

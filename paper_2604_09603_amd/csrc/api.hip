@@ -84,6 +84,35 @@ int32_t echo_gate_sparse(const int32_t* cand_offsets, const int32_t* parent, con
                            as_stream(stream));
 }
 
+size_t echo_gate_elastic_workspace_size(int32_t R, int32_t N, int32_t budget) {
+  if (R < 0 || N < 0 || budget < 0) return 0;
+  return echo::gate_elastic_workspace_bytes(R, N, budget);
+}
+
+int32_t echo_gate_elastic(const int32_t* cand_offsets, const int32_t* parent, const float* logq,
+                          int32_t R, int32_t N, int32_t budget, const int32_t* sig_depth,
+                          const float* log_tau, int32_t num_sig, int32_t w_topk, int32_t w_max,
+                          float* path_score, uint8_t* selected, int32_t* num_selected,
+                          int32_t* trunc_depth, void* workspace, size_t workspace_bytes,
+                          int32_t* status, echo_stream_t stream) {
+  if (R < 1 || N < 0 || budget < 0 || w_topk < 1 || w_max < 0) return ECHO_ERR_INVALID_ARG;
+  if (R > ECHO_MAX_REQUESTS || budget > ECHO_MAX_BUDGET) return ECHO_ERR_UNSUPPORTED;
+  if (!cand_offsets || !num_selected || !workspace) return ECHO_ERR_INVALID_ARG;
+  if (N > 0 && (!parent || !logq || !selected)) return ECHO_ERR_INVALID_ARG;
+  if (num_sig < 0 || num_sig > ECHO_MAX_CHECKPOINTS) return ECHO_ERR_INVALID_ARG;
+  if (num_sig > 0 && (!sig_depth || !log_tau)) return ECHO_ERR_INVALID_ARG;
+  for (int k = 0; k < num_sig; ++k) {
+    if (sig_depth[k] < 1 || sig_depth[k] > ECHO_MAX_DEPTH) return ECHO_ERR_INVALID_ARG;
+    if (log_tau[k] != log_tau[k]) return ECHO_ERR_INVALID_ARG;  // NaN
+  }
+  if (!aligned256(workspace) ||
+      workspace_bytes < echo::gate_elastic_workspace_bytes(R, N, budget))
+    return ECHO_ERR_WORKSPACE;
+  return echo::launch_gate_elastic(cand_offsets, parent, logq, R, N, budget, sig_depth, log_tau,
+                                   num_sig, w_topk, w_max, path_score, selected, num_selected,
+                                   trunc_depth, workspace, status, as_stream(stream));
+}
+
 size_t echo_build_tree_mask_workspace_size(int32_t R, int32_t N, int32_t budget) {
   (void)R;
   (void)N;

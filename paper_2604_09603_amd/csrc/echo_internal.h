@@ -16,6 +16,27 @@ int32_t launch_gate(const int32_t* cand_offsets, const int32_t* parent, const fl
                     hipStream_t stream);
 size_t gate_workspace_bytes(int32_t R, int32_t N, int32_t budget);
 
+// Path scores only (the first gate launch): per candidate the orderable key
+// (0 = never selectable), the clamped parent as a global index (-1: child of
+// the root) and the depth (capped at ECHO_MAX_DEPTH + 1), in the gate workspace.
+struct GateScoreBufs {
+  const uint32_t* keys;
+  const int32_t* pglob;
+  const uint8_t* depth;
+};
+int32_t launch_gate_score(const int32_t* cand_offsets, const int32_t* parent, const float* logq,
+                          int32_t R, int32_t N, float* path_score, void* workspace,
+                          int32_t* status, hipStream_t stream, GateScoreBufs* out);
+
+// Alg. 1 scheduler (checkpoint table as for launch_gate; w_topk >= 1, w_max >= 0).
+int32_t launch_gate_elastic(const int32_t* cand_offsets, const int32_t* parent, const float* logq,
+                            int32_t R, int32_t N, int32_t budget, const int32_t* sig_depth,
+                            const float* log_tau, int32_t num_sig, int32_t w_topk, int32_t w_max,
+                            float* path_score, uint8_t* selected, int32_t* num_selected,
+                            int32_t* trunc_depth, void* workspace, int32_t* status,
+                            hipStream_t stream);
+size_t gate_elastic_workspace_bytes(int32_t R, int32_t N, int32_t budget);
+
 int32_t launch_build_tree_mask(const int32_t* cand_offsets, const int32_t* parent,
                                const int32_t* token, const uint8_t* selected,
                                const int32_t* root_token, const int32_t* prefix_len, int32_t R,

@@ -258,9 +258,14 @@ __global__ __launch_bounds__(kGateThreads) void gate_lmax_clear_kernel(int n, ui
 // maximum key does not exceed the key of ln tau_d (eq. 7; -0 == +0 and -inf
 // has key 0 on both sides, so the key test is the float test S > ln tau).
 __device__ __forceinline__ int first_failed(const SparseArgs& sp, const uint32_t* lmax_r) {
-  for (int d = 1; d <= ECHO_MAX_DEPTH; ++d)
-    if (((sp.mask >> d) & 1u) && !(lmax_r[d] > score_key(sp.lt[d]))) return d;
-  return ECHO_MAX_DEPTH + 1;
+  uint32_t v[kDepths];  // every checkpoint's maximum is loaded before any is tested
+#pragma unroll
+  for (int d = 1; d <= ECHO_MAX_DEPTH; ++d) v[d] = ((sp.mask >> d) & 1u) ? lmax_r[d] : 0u;
+  int t = ECHO_MAX_DEPTH + 1;
+#pragma unroll
+  for (int d = ECHO_MAX_DEPTH; d >= 1; --d)
+    if (((sp.mask >> d) & 1u) && !(v[d] > score_key(sp.lt[d]))) t = d;
+  return t;
 }
 
 // One thread per candidate: keys at or below the request's truncation depth
@@ -274,6 +279,10 @@ __global__ __launch_bounds__(kGateThreads) void gate_trunc_kernel(const int32_t*
   __shared__ uint2 s_red[kGateThreads / kWave];
   __shared__ int s_flag;
   const int g0 = blockIdx.x * kGateThreads;
+  const int g = g0 + threadIdx.x;
+  // this thread's key and depth, fetched while the offsets load
+  uint32_t key = g < N ? ws.keys[g] : 0u;
+  const int dep = g < N ? int(ws.depth[g]) : 0;
   for (int i = threadIdx.x; i <= R; i += kGateThreads) s_offs[i] = cand_offsets[i];
   for (int i = threadIdx.x; i < kHistBins; i += kGateThreads) s_hist[i] = 0u;
   if (threadIdx.x == 0) s_flag = 0;
@@ -298,14 +307,12 @@ __global__ __launch_bounds__(kGateThreads) void gate_trunc_kernel(const int32_t*
       sp.trunc_out[r] = ok ? first_failed(sp, ws.lmax + size_t(r) * kDepths) : ECHO_MAX_DEPTH + 1;
   }
   __syncthreads();
-  const int g = g0 + threadIdx.x;
   if (ok && g < N) {
-    uint32_t key = ws.keys[g];
     if (key != 0u) {
       const int r = upper_bound_idx(s_offs, R + 1, g);
       const int t = r - r0 <= kGateThreads ? int(s_t[r - r0])
                                            : first_failed(sp, ws.lmax + size_t(r) * kDepths);
-      if (int(ws.depth[g]) >= t) {
+      if (dep >= t) {
         key = 0u;
         ws.keys[g] = 0u;
       } else {
@@ -659,6 +666,24 @@ int32_t launch_gate(const int32_t* cand_offsets, const int32_t* parent, const fl
     hipLaunchKernelGGL(gate_finish_kernel, dim3(1), dim3(kGateThreads), 0, stream, N, blocks, ws,
                        selected, status);
   }
+  return hipGetLastError() == hipSuccess ? ECHO_OK : ECHO_ERR_HIP;
+}
+
+int32_t launch_gate_score(const int32_t* cand_offsets, const int32_t* parent, const float* logq,
+                          int32_t R, int32_t N, float* path_score, void* workspace,
+                          int32_t* status, hipStream_t stream, GateScoreBufs* out) {
+  GateWs ws = gate_ws_layout(workspace, N, R);
+  SparseArgs sp{};
+  sp.enabled = 1;  // depths written, no histograms, no checkpoint maxima (mask 0)
+  sp.mask = 0u;
+  for (int d = 0; d < kDepths; ++d) sp.lt[d] = -__builtin_inff();
+  sp.trunc_out = nullptr;
+  const size_t lds = size_t(R + 1) * sizeof(int32_t);
+  hipLaunchKernelGGL(gate_score_kernel, dim3(gate_blocks(N)), dim3(kGateThreads), lds, stream,
+                     cand_offsets, parent, logq, R, N, ws, path_score, status, sp);
+  out->keys = ws.keys;
+  out->pglob = ws.pglob;
+  out->depth = ws.depth;
   return hipGetLastError() == hipSuccess ? ECHO_OK : ECHO_ERR_HIP;
 }
 

@@ -10,8 +10,8 @@ import numpy as np
 import torch
 
 from . import (HEAD_DIM, MAX_DEPTH, echo_accept, echo_build_tree_mask, echo_gate,
-               echo_gate_sparse, echo_tree_verify_attn, gate_workspace_size,
-               tree_verify_attn_workspace_size)
+               echo_gate_elastic, echo_gate_sparse, echo_tree_verify_attn,
+               gate_elastic_workspace_size, gate_workspace_size, tree_verify_attn_workspace_size)
 
 
 def _aligned_workspace(nbytes, device):
@@ -29,12 +29,16 @@ def _dev(a, device, dtype=None):
 
 class VerifyStep:
     """``checkpoints``: optional sequence of (depth, ln tau) pairs; when given the
-    gate stage is echo_gate_sparse (checkpoint truncation, then top-B)."""
+    gate stage is echo_gate_sparse (checkpoint truncation, then top-B).
+    ``elastic``: optional (w_topk, w_max); when given the gate stage is
+    echo_gate_elastic (Alg. 1) with the checkpoints (none if not given)."""
 
-    def __init__(self, batch, device="cuda:0", max_depth=MAX_DEPTH, checkpoints=None):
+    def __init__(self, batch, device="cuda:0", max_depth=MAX_DEPTH, checkpoints=None,
+                 elastic=None):
         cfg = batch["cfg"]
         self.checkpoints = None if checkpoints is None else [(int(d), float(t))
                                                              for d, t in checkpoints]
+        self.elastic = None if elastic is None else (int(elastic[0]), int(elastic[1]))
         self.cfg = cfg
         self.device = device
         self.R = cfg.R
@@ -80,13 +84,21 @@ class VerifyStep:
         self.accept_slots = z32(self.R, max_depth)
         self.bonus_token = z32(self.R)
         self.status = z32(1)
-        self.gate_ws = _aligned_workspace(gate_workspace_size(self.R, self.N, self.B), d)
+        ws_size = (gate_elastic_workspace_size if self.elastic is not None else gate_workspace_size)
+        self.gate_ws = _aligned_workspace(ws_size(self.R, self.N, self.B), d)
         self.attn_ws = _aligned_workspace(
             tree_verify_attn_workspace_size(self.R, self.cap, self.hq, self.hkv, self.D), d)
 
     # ---- the four stages -------------------------------------------------
     def gate(self, stream=None):
-        if self.checkpoints is None:
+        if self.elastic is not None:
+            ck = self.checkpoints or []
+            echo_gate_elastic(self.cand_offsets, self.parent, self.logq, self.R, self.N, self.B,
+                              [d for d, _ in ck], [t for _, t in ck], self.elastic[0],
+                              self.elastic[1], self.path_score, self.selected, self.num_selected,
+                              self.gate_ws, trunc_depth=self.trunc_depth, status=self.status,
+                              stream=stream)
+        elif self.checkpoints is None:
             echo_gate(self.cand_offsets, self.parent, self.logq, self.R, self.N, self.B,
                       self.path_score, self.selected, self.num_selected, self.gate_ws,
                       status=self.status, stream=stream)

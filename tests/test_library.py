@@ -55,6 +55,17 @@ def test_host_side_errors_need_no_gpu():
     assert sparse(None, None, 1) == pkg.ERR_INVALID_ARG
     assert lib.echo_gate_sparse(P(256), P(256), P(256), 1, 1, 4, I(2), F(-1.0), 1, None, P(256),
                                 P(256), None, P(256), ws - 1, None, None) == pkg.ERR_WORKSPACE
+    # elastic scheduler: w_topk < 1, w_max < 0, bad checkpoint, workspace too small
+    wse = lib.echo_gate_elastic_workspace_size(1, 1, 4)
+    assert wse > ws
+    elastic = lambda d, t, n, wt, wm, sz: lib.echo_gate_elastic(
+        P(256), P(256), P(256), 1, 1, 4, d, t, n, wt, wm, None, P(256), P(256), None, P(256), sz,
+        None, None)
+    assert elastic(I(2), F(-1.0), 1, 0, 4, wse) == pkg.ERR_INVALID_ARG
+    assert elastic(I(2), F(-1.0), 1, 2, -1, wse) == pkg.ERR_INVALID_ARG
+    assert elastic(I(0), F(-1.0), 1, 2, 4, wse) == pkg.ERR_INVALID_ARG
+    assert elastic(I(2), F(float("nan")), 1, 2, 4, wse) == pkg.ERR_INVALID_ARG
+    assert elastic(I(2), F(-1.0), 1, 2, 4, wse - 1) == pkg.ERR_WORKSPACE
     assert lib.echo_tree_verify_attn_workspace_size(4, 20, 8, 8, 64) == 0
     assert lib.echo_tree_verify_attn(P(16), P(16), P(16), P(16), P(16), P(16), 10, P(16), P(16), 1,
                                      1, 4, 6, 4, 128, 1.0, P(16), None, P(256), 1 << 30, None,
