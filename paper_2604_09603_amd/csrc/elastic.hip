@@ -48,6 +48,7 @@ struct ElasticWs {
   int32_t* rank;  // [N] rank among its depth's appendable candidates on the trajectory, -1 none
   uint8_t* sel;   // [N] trajectory flags of requests too large for LDS
   int32_t* list;  // [N] appendable lists of requests too large for LDS
+  uint64_t* word; // [N] their rank words
   int32_t* dem;   // [R][kSlots] phase-1 demand per depth on the full-grant trajectory
   int32_t* tdep;  // [R] first failed checkpoint on the trajectory, kNone if none
   int32_t* w2;    // [R] phase-2 demand
@@ -60,7 +61,7 @@ __host__ __device__ inline size_t el_align(size_t x) { return (x + 255) / 256 * 
 
 __host__ inline size_t elastic_own_bytes(int32_t R, int32_t N) {
   return 256 + el_align(size_t(N) * 4) + el_align(size_t(N)) + el_align(size_t(N) * 4) +
-         el_align(size_t(R) * kSlots * 4) + 4 * el_align(size_t(R) * 4);
+         el_align(size_t(N) * 8) + el_align(size_t(R) * kSlots * 4) + 4 * el_align(size_t(R) * 4);
 }
 
 __host__ inline ElasticWs elastic_ws_layout(void* base, int32_t R, int32_t N) {
@@ -74,6 +75,8 @@ __host__ inline ElasticWs elastic_ws_layout(void* base, int32_t R, int32_t N) {
   p += el_align(size_t(N));
   w.list = reinterpret_cast<int32_t*>(p);
   p += el_align(size_t(N) * 4);
+  w.word = reinterpret_cast<uint64_t*>(p);
+  p += el_align(size_t(N) * 8);
   w.dem = reinterpret_cast<int32_t*>(p);
   p += el_align(size_t(R) * kSlots * 4);
   w.tdep = reinterpret_cast<int32_t*>(p);
@@ -89,40 +92,168 @@ __host__ inline ElasticWs elastic_ws_layout(void* base, int32_t R, int32_t N) {
 // ------------------------------------------------------------- request ----
 struct ElasticLds {
   uint32_t key[kElCap];
-  int32_t par[kElCap];  // request-local parent, -1 = the root
+  int32_t par[kElCap];       // request-local parent, -1 = the root
+  uint16_t order[kElCap];    // finite candidates grouped by depth (staged requests)
   uint8_t dep[kElCap];
   uint8_t sel[kElCap];
   int32_t list[kElCap];
+  uint64_t word[kElCap];     // (key, ~index) of each listed candidate: larger = better
+  int off[kSlots + 1];       // start of each depth's group in `order`
+  int fill[kSlots];
   int cnt[2];
   uint32_t mx[2];
   int A[kSlots];    // appendable candidates per depth
   int dem[kSlots];  // phase-1 demand per depth
 };
 
-// The trajectory of request r over its n candidates g = lo + i.  kStaged: the
-// candidates live in LDS; otherwise they are read from the score buffers and
-// the flags and lists live in the workspace.
-template <bool kStaged>
-__device__ void request_trajectory(int r, int lo, int n, const GateScoreBufs& sb,
-                                   const ElasticArgs& ea, const ElasticWs& ew, ElasticLds& L) {
+__device__ __forceinline__ uint64_t rank_word(uint32_t key, int i) {
+  return (uint64_t(key) << 32) | uint64_t(0xFFFFFFFFu - uint32_t(i));
+}
+
+// Rank of every listed candidate among the A listed ones (key descending,
+// local index ascending: the order of their words); the first `dem` are taken.
+// Every lane of a wave reads the same word at a time (an LDS broadcast).
+template <typename Sel>
+__device__ __forceinline__ void rank_level(const int32_t* list, const uint64_t* word, int A,
+                                           int dem, Sel sel, int lo, const ElasticWs& ew) {
+  for (int j = threadIdx.x; j < A; j += kElThreads) {
+    const uint64_t w = word[j];
+    int rank = 0;
+    int m = 0;
+    for (; m + 4 <= A; m += 4)
+      rank += int(word[m] > w) + int(word[m + 1] > w) + int(word[m + 2] > w) +
+              int(word[m + 3] > w);
+    for (; m < A; ++m) rank += int(word[m] > w);
+    const int i = list[j];
+    ew.rank[lo + i] = rank;
+    if (rank < dem) sel(i);
+  }
+}
+
+// Per-request results of the trajectory (thread 0): demands, first failed
+// checkpoint t and the phase-2 demand at depth t - 1.
+__device__ __forceinline__ void write_trajectory(int r, int t, const ElasticArgs& ea,
+                                                 const ElasticWs& ew, const ElasticLds& L) {
+  ew.dem[size_t(r) * kSlots] = 0;
+  for (int d = 1; d <= ECHO_MAX_DEPTH; ++d) ew.dem[size_t(r) * kSlots + d] = L.dem[d];
+  ew.tdep[r] = t;
+  int w = 0;
+  if (t >= 2 && t <= ECHO_MAX_DEPTH) {
+    const int l = t - 1;
+    w = max(0, min(ea.w_max - L.dem[l], L.A[l] - L.dem[l]));
+  }
+  ew.w2[r] = w;
+}
+
+// One depth of the trajectory after its appendable list is built: the
+// checkpoint test (eq. 7 on keys: order-preserving, -0 == +0, -inf -> 0) and
+// the demand.  Returns false when the walk stops (t set on a failed test).
+__device__ __forceinline__ bool level_test(int d, int A, uint32_t mx, const ElasticArgs& ea,
+                                           int* t) {
+  if (((ea.mask >> d) & 1u) && !(mx > score_key(ea.lt[d]))) {
+    *t = d;
+    return false;
+  }
+  return A > 0;  // none appendable: the drafted tree is exhausted
+}
+
+// Trajectory of a request whose candidates fit in LDS: they are grouped by
+// depth once, so each depth visits only its own candidates.
+__device__ void trajectory_staged(int r, int lo, int n, const GateScoreBufs& sb,
+                                  const ElasticArgs& ea, const ElasticWs& ew, ElasticLds& L) {
   const int tid = threadIdx.x;
-  uint8_t* SEL = kStaged ? L.sel : ew.sel + lo;
-  int32_t* LIST = kStaged ? L.list : ew.list + lo;
-  auto keyf = [&](int i) -> uint32_t { return kStaged ? L.key[i] : sb.keys[lo + i]; };
-  auto depf = [&](int i) -> int { return kStaged ? int(L.dep[i]) : int(sb.depth[lo + i]); };
-  auto parf = [&](int i) -> int {
-    if (kStaged) return L.par[i];
-    const int p = sb.pglob[lo + i];
-    return p < 0 ? -1 : p - lo;
-  };
-  for (int i = tid; i < n; i += kElThreads) {
-    if (kStaged) {
-      L.key[i] = sb.keys[lo + i];
-      const int p = sb.pglob[lo + i];
-      L.par[i] = p < 0 ? -1 : p - lo;
-      L.dep[i] = sb.depth[lo + i];
+  if (tid <= kSlots) L.off[tid] = 0;
+  if (tid < kSlots) {
+    L.fill[tid] = 0;
+    L.A[tid] = 0;
+    L.dem[tid] = 0;
+  }
+  if (tid < 2) {
+    L.cnt[tid] = 0;
+    L.mx[tid] = 0u;
+  }
+  __syncthreads();
+  // all of this thread's candidates are fetched before any is stored, so the
+  // loads overlap instead of paying the memory latency once per candidate
+  constexpr int kPer = kElCap / kElThreads;
+  uint32_t kk[kPer];
+  int pp[kPer], dd[kPer];
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const int i = tid + q * kElThreads;
+    kk[q] = i < n ? sb.keys[lo + i] : 0u;
+    pp[q] = i < n ? sb.pglob[lo + i] : -1;
+    dd[q] = i < n ? int(sb.depth[lo + i]) : 0;
+  }
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const int i = tid + q * kElThreads;
+    if (i < n) {
+      L.key[i] = kk[q];
+      L.par[i] = pp[q] < 0 ? -1 : pp[q] - lo;
+      L.dep[i] = uint8_t(dd[q]);
+      L.sel[i] = 0;
+      ew.rank[lo + i] = -1;
+      if (kk[q] != 0u) atomicAdd(&L.off[dd[q] + 1], 1);  // finite keys have depth <= 16
     }
-    SEL[i] = 0;
+  }
+  __syncthreads();
+  if (tid < kWave) {  // inclusive scan of the depth counts (18 entries) in one wave
+    int v = tid <= kSlots ? L.off[tid] : 0;
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) {
+      const int u = __shfl_up(v, o, kWave);
+      if (tid >= o) v += u;
+    }
+    if (tid <= kSlots) L.off[tid] = v;
+  }
+  __syncthreads();
+  for (int i = tid; i < n; i += kElThreads) {
+    if (L.key[i] == 0u) continue;
+    const int d = L.dep[i];
+    L.order[L.off[d] + atomicAdd(&L.fill[d], 1)] = uint16_t(i);
+  }
+  __syncthreads();
+  int t = kNone;
+  int par = 0;
+  for (int d = 1; d <= ECHO_MAX_DEPTH; ++d) {
+    for (int j = L.off[d] + tid; j < L.off[d + 1]; j += kElThreads) {
+      const int i = L.order[j];
+      const int p = L.par[i];
+      if (p >= 0 && !L.sel[p]) continue;
+      const uint32_t k = L.key[i];
+      const int j2 = atomicAdd(&L.cnt[par], 1);
+      L.list[j2] = i;
+      L.word[j2] = rank_word(k, i);
+      atomicMax(&L.mx[par], k);
+    }
+    __syncthreads();
+    const int A = L.cnt[par];
+    if (!level_test(d, A, L.mx[par], ea, &t)) break;
+    const int dem = min(ea.w_topk, A);
+    rank_level(L.list, L.word, A, dem, [&](int i) { L.sel[i] = 1; }, lo, ew);
+    if (tid == 0) {
+      L.A[d] = A;
+      L.dem[d] = dem;
+      L.cnt[par ^ 1] = 0;
+      L.mx[par ^ 1] = 0u;
+    }
+    __syncthreads();
+    par ^= 1;
+  }
+  if (tid == 0) write_trajectory(r, t, ea, ew, L);
+}
+
+// Trajectory of a request too large for LDS: flags and lists in the workspace,
+// every depth scans the request's candidates.
+__device__ void trajectory_global(int r, int lo, int n, const GateScoreBufs& sb,
+                                  const ElasticArgs& ea, const ElasticWs& ew, ElasticLds& L) {
+  const int tid = threadIdx.x;
+  uint8_t* sel = ew.sel + lo;
+  int32_t* list = ew.list + lo;
+  uint64_t* word = ew.word + lo;
+  for (int i = tid; i < n; i += kElThreads) {
+    sel[i] = 0;
     ew.rank[lo + i] = -1;
   }
   if (tid < kSlots) {
@@ -137,40 +268,22 @@ __device__ void request_trajectory(int r, int lo, int n, const GateScoreBufs& sb
   int t = kNone;
   int par = 0;
   for (int d = 1; d <= ECHO_MAX_DEPTH; ++d) {
-    // appendable depth-d candidates: finite, parent held (or the root)
     for (int i = tid; i < n; i += kElThreads) {
-      if (depf(i) != d) continue;
-      const uint32_t k = keyf(i);
+      if (int(sb.depth[lo + i]) != d) continue;
+      const uint32_t k = sb.keys[lo + i];
       if (k == 0u) continue;
-      const int p = parf(i);
-      if (p >= 0 && !SEL[p]) continue;
-      LIST[atomicAdd(&L.cnt[par], 1)] = i;
+      const int p = sb.pglob[lo + i];
+      if (p >= 0 && !sel[p - lo]) continue;
+      const int j2 = atomicAdd(&L.cnt[par], 1);
+      list[j2] = i;
+      word[j2] = rank_word(k, i);
       atomicMax(&L.mx[par], k);
     }
     __syncthreads();
     const int A = L.cnt[par];
-    const uint32_t mx = L.mx[par];
-    // eq. 7: the largest appendable path score strictly above ln tau (keys are
-    // order-preserving, -0 == +0, -inf has key 0)
-    const bool pass = !((ea.mask >> d) & 1u) || mx > score_key(ea.lt[d]);
-    if (!pass) {
-      t = d;
-      break;
-    }
-    if (A == 0) break;  // drafted tree exhausted
+    if (!level_test(d, A, L.mx[par], ea, &t)) break;
     const int dem = min(ea.w_topk, A);
-    for (int j = tid; j < A; j += kElThreads) {
-      const int i = LIST[j];
-      const uint32_t k = keyf(i);
-      int rank = 0;
-      for (int m = 0; m < A; ++m) {
-        const int o = LIST[m];
-        const uint32_t ko = keyf(o);
-        rank += (ko > k || (ko == k && o < i)) ? 1 : 0;
-      }
-      ew.rank[lo + i] = rank;
-      if (rank < dem) SEL[i] = 1;
-    }
+    rank_level(list, word, A, dem, [&](int i) { sel[i] = 1; }, lo, ew);
     if (tid == 0) {
       L.A[d] = A;
       L.dem[d] = dem;
@@ -180,17 +293,7 @@ __device__ void request_trajectory(int r, int lo, int n, const GateScoreBufs& sb
     __syncthreads();
     par ^= 1;
   }
-  if (tid == 0) {
-    ew.dem[size_t(r) * kSlots] = 0;
-    for (int d = 1; d <= ECHO_MAX_DEPTH; ++d) ew.dem[size_t(r) * kSlots + d] = L.dem[d];
-    ew.tdep[r] = t;
-    int w = 0;
-    if (t >= 2 && t <= ECHO_MAX_DEPTH) {
-      const int l = t - 1;
-      w = max(0, min(ea.w_max - L.dem[l], L.A[l] - L.dem[l]));
-    }
-    ew.w2[r] = w;
-  }
+  if (tid == 0) write_trajectory(r, t, ea, ew, L);
 }
 
 __global__ __launch_bounds__(kElThreads) void elastic_request_kernel(
@@ -203,8 +306,8 @@ __global__ __launch_bounds__(kElThreads) void elastic_request_kernel(
   // range in bounds
   if (lo < 0 || hi > N || hi < lo) lo = hi = 0;
   const int n = hi - lo;
-  if (n <= kElCap) request_trajectory<true>(r, lo, n, sb, ea, ew, L);
-  else request_trajectory<false>(r, lo, n, sb, ea, ew, L);
+  if (n <= kElCap) trajectory_staged(r, lo, n, sb, ea, ew, L);
+  else trajectory_global(r, lo, n, sb, ea, ew, L);
 }
 
 // -------------------------------------------------------------- finish ----
@@ -213,42 +316,57 @@ __global__ __launch_bounds__(kFinThreads) void elastic_finish_kernel(int R, int 
                                                                     int32_t* __restrict__ num_selected,
                                                                     int32_t* __restrict__ trunc_out) {
   constexpr int NW = kFinThreads / kWave;
-  __shared__ int s_tot[NW][kSlots];
+  __shared__ int s_tot[kFinThreads][kSlots];  // per-thread demands, summed by column
+  __shared__ int s_col[kSlots];
   __shared__ int s_scan[NW + 1];
   __shared__ int s_cut, s_left;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
-  // 1. total phase-1 demand per depth
-  int tot[kSlots];
+  // 1. total phase-1 demand per depth; the first request of each thread is
+  // kept in registers for step 3
+  const int tdep0 = tid < R ? ew.tdep[tid] : kNone;
+  const int w20 = tid < R ? ew.w2[tid] : 0;
+  int dem0[kSlots], tot[kSlots];
 #pragma unroll
-  for (int d = 0; d < kSlots; ++d) tot[d] = 0;
-  for (int r = tid; r < R; r += kFinThreads) {
+  for (int d = 0; d < kSlots; ++d) {
+    dem0[d] = (d > 0 && tid < R) ? ew.dem[size_t(tid) * kSlots + d] : 0;
+    tot[d] = dem0[d];
+  }
+  for (int r = tid + kFinThreads; r < R; r += kFinThreads) {
 #pragma unroll
     for (int d = 1; d < kSlots; ++d) tot[d] += ew.dem[size_t(r) * kSlots + d];
   }
+  // column sums through LDS: wave w adds depth w + 1 over all threads
+  static_assert(kFinThreads / kWave == ECHO_MAX_DEPTH, "one wave per depth");
 #pragma unroll
-  for (int d = 1; d < kSlots; ++d) {
-    int v = tot[d];
+  for (int d = 1; d < kSlots; ++d) s_tot[tid][d] = tot[d];
+  __syncthreads();
+  {
+    const int d = wid + 1;
+    int v = 0;
+#pragma unroll
+    for (int k = 0; k < kFinThreads / kWave; ++k) v += s_tot[lane + kWave * k][d];
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
-    if (lane == 0) s_tot[wid][d] = v;
+    if (lane == 0) s_col[d] = v;
   }
   __syncthreads();
   // 2. the depth loop of phase 1 runs while budget is left; the cut is the
   // first depth whose demands reach what is left: there the budget runs out
   // (exactly, or part way), and the requests after that point are not tested
-  if (tid == 0) {
+  if (tid < kWave) {
     int left = budget, cut = kNone;
+#pragma unroll
     for (int d = 1; d <= ECHO_MAX_DEPTH; ++d) {
-      int T = 0;
-      for (int w = 0; w < NW; ++w) T += s_tot[w][d];
-      if (T >= left) {
-        cut = d;
-        break;
+      const int Td = s_col[d];
+      if (cut == kNone) {
+        if (Td >= left) cut = d;
+        else left -= Td;
       }
-      left -= T;
     }
-    s_cut = cut;
-    s_left = left;
+    if (tid == 0) {
+      s_cut = cut;
+      s_left = left;
+    }
   }
   __syncthreads();
   const int cut = s_cut;
@@ -259,14 +377,20 @@ __global__ __launch_bounds__(kFinThreads) void elastic_finish_kernel(int R, int 
     // all (and can be truncated there) only while budget remains at its turn
     for (int r0 = 0; r0 < R; r0 += kFinThreads) {
       const int r = r0 + tid;
-      const int v = r < R ? ew.dem[size_t(r) * kSlots + cut] : 0;
+      int v = 0;
+      if (r0 == 0) {
+#pragma unroll
+        for (int d = 1; d < kSlots; ++d) v = d == cut ? dem0[d] : v;
+      } else if (r < R) {
+        v = ew.dem[size_t(r) * kSlots + cut];
+      }
       int tot_c;
       const int excl = run + block_exclusive_sum<kFinThreads>(v, s_scan, &tot_c);
       if (r < R) {
         ew.g1[r] = max(0, min(v, left - excl));
         ew.g2[r] = 0;
         if (trunc_out != nullptr) {
-          const int td = ew.tdep[r];
+          const int td = r0 == 0 ? tdep0 : ew.tdep[r];
           trunc_out[r] = (td < cut || (td == cut && excl < left)) ? td : kNone;
         }
       }
@@ -280,13 +404,13 @@ __global__ __launch_bounds__(kFinThreads) void elastic_finish_kernel(int R, int 
     // phase 2: truncated requests in order widen with what is left
     for (int r0 = 0; r0 < R; r0 += kFinThreads) {
       const int r = r0 + tid;
-      const int v = r < R ? ew.w2[r] : 0;
+      const int v = r0 == 0 ? w20 : (r < R ? ew.w2[r] : 0);
       int tot_c;
       const int excl = run + block_exclusive_sum<kFinThreads>(v, s_scan, &tot_c);
       if (r < R) {
         ew.g1[r] = 0;
         ew.g2[r] = max(0, min(v, left - excl));
-        if (trunc_out != nullptr) trunc_out[r] = ew.tdep[r];
+        if (trunc_out != nullptr) trunc_out[r] = r0 == 0 ? tdep0 : ew.tdep[r];
       }
       run += tot_c;
     }
@@ -306,25 +430,27 @@ __global__ __launch_bounds__(kSelThreads) void elastic_select_kernel(
   __syncthreads();
   const int g = blockIdx.x * kSelThreads + threadIdx.x;
   const int cut = ew.meta[0];
+  // the selection rule, with each round of independent loads issued together
   auto is_sel = [&](int x) -> bool {
-    if (sb.keys[x] == 0u) return false;  // also every candidate of a malformed CSR
+    const uint32_t key = sb.keys[x];
     const int rk = ew.rank[x];
-    if (rk < 0) return false;
-    const int r = upper_bound_idx(s_offs, R + 1, x);
     const int d = int(sb.depth[x]);
-    const int dm = ew.dem[size_t(r) * kSlots + d];
+    if (key == 0u || rk < 0) return false;  // also every candidate of a malformed CSR
+    const int r = upper_bound_idx(s_offs, R + 1, x);
+    const int dm = ew.dem[size_t(r) * kSlots + d];  // d <= 16: the key is finite
+    const int a = ew.g1[r];
+    const int b = ew.g2[r];
+    const int td = ew.tdep[r];
     if (d < cut && rk < dm) return true;
-    if (d == cut && rk < ew.g1[r]) return true;
-    return cut == kNone && d == ew.tdep[r] - 1 && rk >= dm && rk < dm + ew.g2[r];
+    if (d == cut && rk < a) return true;
+    return cut == kNone && d == td - 1 && rk >= dm && rk < dm + b;
   };
   int bits = 0;
   if (g < N) {
+    const int p = sb.pglob[g];
     const bool s = is_sel(g);
     selected[g] = s ? 1 : 0;
-    if (s) {
-      const int p = sb.pglob[g];
-      if (p >= 0 && !is_sel(p)) bits |= ECHO_DATA_NOT_CLOSED;
-    }
+    if (s && p >= 0 && !is_sel(p)) bits |= ECHO_DATA_NOT_CLOSED;
   }
   wave_status_or(status, bits);
 }
