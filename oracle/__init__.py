@@ -21,6 +21,9 @@ Stages (each module cites the passage it follows):
 * ``attn``   -- tree-masked grouped-query attention of every verify slot over
                its request's KV prefix plus its in-tree ancestors, in float64
                (the single parallel verification forward of Section 3.1).
+* ``serve``  -- the serving step around the path: target argmax feeding
+               acceptance, KV commit of the accepted path into a paged cache,
+               verification attention over that paged cache.
 * ``accept`` -- greedy (temperature 0) acceptance of the longest draft path
                matching the target argmax (Section 2, standard SD).
 
@@ -34,3 +37,4 @@ from .elastic import elastic_schedule
 from .mask import build_tree_mask
 from .attn import tree_verify_attn
 from .accept import accept
+from .serve import target_argmax, accept_from_logits, tree_verify_attn_paged, commit_kv
