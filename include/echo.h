@@ -236,6 +236,31 @@ size_t echo_tree_verify_attn_workspace_size(int32_t R, int32_t max_rows, int32_t
                                             int32_t num_kv_heads, int32_t head_dim);
 
 /*
+ * echo_tree_verify_attn_paged -- echo_tree_verify_attn with each request's KV
+ * prefix in a paged cache (the block-table layout of serving engines; the
+ * paper leaves the cache layout to the engine).
+ *
+ * Position p < prefix_len[r] of request r is row p % page_size of page
+ * block_table[r * max_pages_per_request + p / page_size]; a page holds
+ * page_size token rows of Hkv * 128 bf16 each.
+ *   k_pages, v_pages [num_pages][page_size][Hkv][128] bf16
+ *   page_size        power of two, >= 32 (a 32-key tile never straddles pages)
+ *   block_table      [R][max_pages_per_request] int32 page ids
+ *   prefix_len       [R] int32 cached positions per request
+ * A request whose prefix needs a page id outside [0, num_pages) (or a length
+ * beyond its block-table row) is skipped with ECHO_DATA_BAD_OFFSETS, like an
+ * invalid kv_offsets range.  Everything else is as for echo_tree_verify_attn,
+ * including the workspace size.
+ */
+int32_t echo_tree_verify_attn_paged(
+    const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new, const uint16_t* k_pages,
+    const uint16_t* v_pages, int64_t num_pages, int32_t page_size, const int32_t* block_table,
+    int32_t max_pages_per_request, const int32_t* prefix_len, const int32_t* q_offsets,
+    const uint32_t* tree_mask, int32_t mask_words, int32_t R, int32_t max_rows,
+    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, float sm_scale, float* out,
+    float* lse, void* workspace, size_t workspace_bytes, int32_t* status, echo_stream_t stream);
+
+/*
  * echo_accept -- greedy acceptance (Section 2 standard SD, greedy decoding).
  *
  * Root slot valid; slot s valid iff its parent is valid, its depth <=
@@ -253,6 +278,46 @@ int32_t echo_accept(const int32_t* q_offsets, const int32_t* slot_parent,
                     int32_t max_rows, int32_t max_depth, int32_t* accept_len,
                     int32_t* accept_slots, int32_t* bonus_token, int32_t* status,
                     echo_stream_t stream);
+
+/*
+ * echo_accept_logits -- echo_accept with the target tokens taken from the
+ * target model's logits: the greedy (temperature 0) token after slot s is the
+ * argmax of logits[s][0 .. vocab), compared as floats (-0 == +0), NaN never
+ * winning over a number, ties to the smaller token id (a row of NaN gives 0).
+ *   logits       [max_rows][vocab] bf16, row-major
+ *   target_token [max_rows] int32  OUTPUT: the argmax of every existing row
+ * The other arguments and outputs are those of echo_accept.  The argmax reads
+ * q_offsets[R] * vocab * 2 bytes: it is bound by HBM bandwidth.
+ */
+int32_t echo_accept_logits(const int32_t* q_offsets, const int32_t* slot_parent,
+                           const int32_t* slot_token, const uint16_t* logits, int64_t vocab,
+                           int32_t R, int32_t max_rows, int32_t max_depth, int32_t* target_token,
+                           int32_t* accept_len, int32_t* accept_slots, int32_t* bonus_token,
+                           int32_t* status, echo_stream_t stream);
+
+/*
+ * echo_commit_kv -- append each request's verified root and accepted path to
+ * its paged KV cache (the step after acceptance; the paper leaves the cache
+ * to the serving engine).
+ *
+ * For a request with verify slots, rows k_new/v_new[q_offsets[r]] (the root)
+ * and k_new/v_new[accept_slots[r][j]], j < accept_len[r], are written at
+ * positions prefix_len[r], prefix_len[r] + 1, ... (page layout as for
+ * echo_tree_verify_attn_paged), and prefix_len[r] grows by 1 + accept_len[r]
+ * (in place).  The caller provides the pages: if a position needs a page id
+ * outside [0, num_pages), or a slot index is outside [0, max_rows), nothing
+ * of that request is written (ECHO_DATA_BAD_OFFSETS).  Requests without slots
+ * are left unchanged.
+ *   accept_len [R], accept_slots [R][max_depth]  as written by echo_accept
+ *   k_new, v_new [max_rows][Hkv][128] bf16; k_pages, v_pages as above
+ *   page_size   any positive size; pointers 16-byte aligned
+ */
+int32_t echo_commit_kv(const int32_t* q_offsets, const int32_t* accept_len,
+                       const int32_t* accept_slots, int32_t max_depth, const uint16_t* k_new,
+                       const uint16_t* v_new, int32_t R, int32_t max_rows, int32_t num_kv_heads,
+                       uint16_t* k_pages, uint16_t* v_pages, int64_t num_pages, int32_t page_size,
+                       const int32_t* block_table, int32_t max_pages_per_request,
+                       int32_t* prefix_len, int32_t* status, echo_stream_t stream);
 
 /*
  * echo_set_attn_profile_events -- measurement hook (not a step of the method).

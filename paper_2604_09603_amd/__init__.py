@@ -36,6 +36,7 @@ EXPORTS = [
     "echo_gate_elastic", "echo_gate_elastic_workspace_size",
     "echo_build_tree_mask", "echo_build_tree_mask_workspace_size",
     "echo_tree_verify_attn", "echo_tree_verify_attn_workspace_size",
+    "echo_tree_verify_attn_paged", "echo_accept_logits", "echo_commit_kv",
     "echo_accept", "echo_set_attn_profile_events", "echo_status_string", "echo_version",
 ]
 
@@ -63,6 +64,13 @@ _SIGS = {
                                      _I32, _I32, _F32, _P, _P, _P, _SZ, _P, _P]),
     "echo_tree_verify_attn_workspace_size": (_SZ, [_I32, _I32, _I32, _I32, _I32]),
     "echo_accept": (_I32, [_P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P]),
+    "echo_tree_verify_attn_paged": (_I32, [_P, _P, _P, _P, _P, _I64, _I32, _P, _I32, _P, _P, _P,
+                                           _I32, _I32, _I32, _I32, _I32, _I32, _F32, _P, _P, _P,
+                                           _SZ, _P, _P]),
+    "echo_accept_logits": (_I32, [_P, _P, _P, _P, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P,
+                                  _P]),
+    "echo_commit_kv": (_I32, [_P, _P, _P, _I32, _P, _P, _I32, _I32, _I32, _P, _P, _I64, _I32, _P,
+                              _I32, _P, _P, _P]),
     "echo_set_attn_profile_events": (_I32, [_P, _P]),
     "echo_status_string": (ctypes.c_char_p, [_I32]),
     "echo_version": (ctypes.c_char_p, []),
@@ -235,4 +243,48 @@ def echo_accept(q_offsets, slot_parent, slot_token, target_token, R, max_rows, m
                               _stream(stream))
     if check:
         _check(code, "echo_accept")
+    return code
+
+
+def echo_tree_verify_attn_paged(q, k_new, v_new, k_pages, v_pages, page_size, block_table,
+                                prefix_len, q_offsets, tree_mask, mask_words, R, max_rows, hq,
+                                hkv, head_dim, sm_scale, out, lse, workspace, status=None,
+                                stream=None, check=True):
+    """Verification attention over a paged KV cache.  Device tensors; k_pages is
+    [num_pages, page_size, Hkv, 128] bf16 bits, block_table [R, max_pages]."""
+    code = load().echo_tree_verify_attn_paged(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pages), _ptr(v_pages), k_pages.shape[0],
+        page_size, _ptr(block_table), block_table.shape[1], _ptr(prefix_len), _ptr(q_offsets),
+        _ptr(tree_mask), mask_words, R, max_rows, hq, hkv, head_dim, sm_scale, _ptr(out),
+        _ptr(lse), _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(status),
+        _stream(stream))
+    if check:
+        _check(code, "echo_tree_verify_attn_paged")
+    return code
+
+
+def echo_accept_logits(q_offsets, slot_parent, slot_token, logits, R, max_rows, max_depth,
+                       target_token, accept_len, accept_slots, bonus_token, status=None,
+                       stream=None, check=True):
+    """Target argmax of bf16 logits [max_rows, V] followed by greedy acceptance."""
+    code = load().echo_accept_logits(_ptr(q_offsets), _ptr(slot_parent), _ptr(slot_token),
+                                     _ptr(logits), logits.shape[1], R, max_rows, max_depth,
+                                     _ptr(target_token), _ptr(accept_len), _ptr(accept_slots),
+                                     _ptr(bonus_token), _ptr(status), _stream(stream))
+    if check:
+        _check(code, "echo_accept_logits")
+    return code
+
+
+def echo_commit_kv(q_offsets, accept_len, accept_slots, max_depth, k_new, v_new, R, max_rows,
+                   hkv, k_pages, v_pages, page_size, block_table, prefix_len, status=None,
+                   stream=None, check=True):
+    """Append each request's root and accepted slots to its paged KV cache."""
+    code = load().echo_commit_kv(_ptr(q_offsets), _ptr(accept_len), _ptr(accept_slots),
+                                 max_depth, _ptr(k_new), _ptr(v_new), R, max_rows, hkv,
+                                 _ptr(k_pages), _ptr(v_pages), k_pages.shape[0], page_size,
+                                 _ptr(block_table), block_table.shape[1], _ptr(prefix_len),
+                                 _ptr(status), _stream(stream))
+    if check:
+        _check(code, "echo_commit_kv")
     return code

@@ -177,7 +177,7 @@ int32_t echo_tree_verify_attn(const uint16_t* q, const uint16_t* k_new, const ui
                         reinterpret_cast<uintptr_t>(v_cache) | reinterpret_cast<uintptr_t>(out);
   if (mis & 15u) return ECHO_ERR_INVALID_ARG;
   if (max_rows == 0) return ECHO_OK;
-  echo::AttnArgs a;
+  echo::AttnArgs a{};
   a.q = q;
   a.k_new = k_new;
   a.v_new = v_new;
@@ -185,6 +185,62 @@ int32_t echo_tree_verify_attn(const uint16_t* q, const uint16_t* k_new, const ui
   a.v_cache = v_cache;
   a.kv_offsets = kv_offsets;
   a.kv_rows = kv_rows;
+  a.q_offsets = q_offsets;
+  a.tree_mask = tree_mask;
+  a.mask_words = mask_words;
+  a.R = R;
+  a.max_rows = max_rows;
+  a.hq = num_q_heads;
+  a.hkv = num_kv_heads;
+  a.sm_scale = sm_scale;
+  a.out = out;
+  a.lse = lse;
+  a.workspace = workspace;
+  a.status = status;
+  return echo::launch_tree_verify_attn(a, as_stream(stream));
+}
+
+int32_t echo_tree_verify_attn_paged(
+    const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new, const uint16_t* k_pages,
+    const uint16_t* v_pages, int64_t num_pages, int32_t page_size, const int32_t* block_table,
+    int32_t max_pages_per_request, const int32_t* prefix_len, const int32_t* q_offsets,
+    const uint32_t* tree_mask, int32_t mask_words, int32_t R, int32_t max_rows,
+    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, float sm_scale, float* out,
+    float* lse, void* workspace, size_t workspace_bytes, int32_t* status, echo_stream_t stream) {
+  if (R < 1 || max_rows < 0 || num_q_heads < 1 || num_kv_heads < 1 || mask_words < 1 ||
+      num_pages < 1 || max_pages_per_request < 1)
+    return ECHO_ERR_INVALID_ARG;
+  if (num_q_heads % num_kv_heads != 0) return ECHO_ERR_INVALID_ARG;
+  // a page holds whole 32-key tiles and a power-of-two number of rows
+  if (page_size < 32 || (page_size & (page_size - 1)) != 0) return ECHO_ERR_UNSUPPORTED;
+  if (head_dim != ECHO_HEAD_DIM || R > ECHO_MAX_REQUESTS) return ECHO_ERR_UNSUPPORTED;
+  if (num_pages * int64_t(page_size) >= (int64_t(1) << 31)) return ECHO_ERR_UNSUPPORTED;
+  if (int64_t(max_pages_per_request) * page_size >= (int64_t(1) << 31)) return ECHO_ERR_UNSUPPORTED;
+  if (int64_t(max_rows) * num_q_heads >= (int64_t(1) << 26)) return ECHO_ERR_UNSUPPORTED;
+  if (!q || !k_new || !v_new || !k_pages || !v_pages || !block_table || !prefix_len ||
+      !q_offsets || !tree_mask || !out || !workspace)
+    return ECHO_ERR_INVALID_ARG;
+  if (!aligned256(workspace) ||
+      workspace_bytes < echo::attn_workspace_bytes(R, max_rows, num_q_heads, num_kv_heads))
+    return ECHO_ERR_WORKSPACE;
+  const uintptr_t mis = reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k_new) |
+                        reinterpret_cast<uintptr_t>(v_new) | reinterpret_cast<uintptr_t>(k_pages) |
+                        reinterpret_cast<uintptr_t>(v_pages) | reinterpret_cast<uintptr_t>(out);
+  if (mis & 15u) return ECHO_ERR_INVALID_ARG;
+  if (max_rows == 0) return ECHO_OK;
+  echo::AttnArgs a{};
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_cache = k_pages;
+  a.v_cache = v_pages;
+  a.kv_offsets = nullptr;
+  a.kv_rows = 0;
+  a.block_table = block_table;
+  a.prefix_len = prefix_len;
+  a.page_size = page_size;
+  a.max_pages = max_pages_per_request;
+  a.num_pages = num_pages;
   a.q_offsets = q_offsets;
   a.tree_mask = tree_mask;
   a.mask_words = mask_words;
@@ -233,5 +289,48 @@ const char* echo_status_string(int32_t code) {
 }
 
 const char* echo_version(void) { return "echo-mi355x 0.1.0 (gfx950)"; }
+
+}  // extern "C"
+
+extern "C" {
+
+int32_t echo_accept_logits(const int32_t* q_offsets, const int32_t* slot_parent,
+                           const int32_t* slot_token, const uint16_t* logits, int64_t vocab,
+                           int32_t R, int32_t max_rows, int32_t max_depth, int32_t* target_token,
+                           int32_t* accept_len, int32_t* accept_slots, int32_t* bonus_token,
+                           int32_t* status, echo_stream_t stream) {
+  if (R < 1 || max_rows < 0 || vocab < 1 || vocab > 0x7FFFFFFF) return ECHO_ERR_INVALID_ARG;
+  if (max_depth < 1 || max_depth > ECHO_MAX_DEPTH || R > ECHO_MAX_REQUESTS)
+    return ECHO_ERR_UNSUPPORTED;
+  if (!q_offsets || !accept_len || !accept_slots || !bonus_token || !target_token)
+    return ECHO_ERR_INVALID_ARG;
+  if (max_rows > 0 && (!slot_parent || !slot_token || !logits)) return ECHO_ERR_INVALID_ARG;
+  return echo::launch_accept_logits(q_offsets, slot_parent, slot_token, logits, vocab, R,
+                                    max_rows, max_depth, target_token, accept_len, accept_slots,
+                                    bonus_token, status, as_stream(stream));
+}
+
+int32_t echo_commit_kv(const int32_t* q_offsets, const int32_t* accept_len,
+                       const int32_t* accept_slots, int32_t max_depth, const uint16_t* k_new,
+                       const uint16_t* v_new, int32_t R, int32_t max_rows, int32_t num_kv_heads,
+                       uint16_t* k_pages, uint16_t* v_pages, int64_t num_pages, int32_t page_size,
+                       const int32_t* block_table, int32_t max_pages_per_request,
+                       int32_t* prefix_len, int32_t* status, echo_stream_t stream) {
+  if (R < 1 || max_rows < 0 || num_kv_heads < 1 || num_pages < 1 || page_size < 1 ||
+      max_pages_per_request < 1)
+    return ECHO_ERR_INVALID_ARG;
+  if (max_depth < 1 || max_depth > ECHO_MAX_DEPTH || R > ECHO_MAX_REQUESTS)
+    return ECHO_ERR_UNSUPPORTED;
+  if (!q_offsets || !accept_len || !accept_slots || !k_new || !v_new || !k_pages || !v_pages ||
+      !block_table || !prefix_len)
+    return ECHO_ERR_INVALID_ARG;
+  const uintptr_t al = reinterpret_cast<uintptr_t>(k_new) | reinterpret_cast<uintptr_t>(v_new) |
+                       reinterpret_cast<uintptr_t>(k_pages) | reinterpret_cast<uintptr_t>(v_pages);
+  if (al & 15) return ECHO_ERR_INVALID_ARG;
+  return echo::launch_commit_kv(q_offsets, accept_len, accept_slots, max_depth, k_new, v_new, R,
+                                max_rows, num_kv_heads, k_pages, v_pages, num_pages, page_size,
+                                block_table, max_pages_per_request, prefix_len, status,
+                                as_stream(stream));
+}
 
 }  // extern "C"

@@ -142,11 +142,39 @@ __device__ __forceinline__ Stream stream_of(const Unit& u, int w, int hkv, int G
 }
 
 // ---------------------------------------------------------------- plan ----
-__device__ __forceinline__ bool request_ok(const int32_t* q_offsets, const int64_t* kv_offsets,
-                                           long long kv_rows, int max_rows, int r) {
+// Where the requests' KV prefixes live: rows [kv_offsets[r], kv_offsets[r+1])
+// of a token-major cache, or (block_table != nullptr) prefix_len[r] positions
+// read through the request's row of the block table.
+struct KvSource {
+  const int64_t* kv_offsets;
+  long long kv_rows;
+  const int32_t* block_table;
+  const int32_t* prefix_len;
+  int page_size;
+  int max_pages;
+  long long num_pages;
+};
+
+// Slot range and prefix of request r are usable (every page of a paged prefix
+// present and in range).
+__device__ __forceinline__ bool request_ok(const int32_t* q_offsets, const KvSource& kv,
+                                           int max_rows, int r) {
   const int q0 = q_offsets[r], q1 = q_offsets[r + 1];
-  const long long k0 = kv_offsets[r], k1 = kv_offsets[r + 1];
-  return q0 >= 0 && q1 >= q0 && q1 <= max_rows && k0 >= 0 && k1 >= k0 && k1 <= kv_rows;
+  if (!(q0 >= 0 && q1 >= q0 && q1 <= max_rows)) return false;
+  if (kv.block_table == nullptr) {
+    const long long k0 = kv.kv_offsets[r], k1 = kv.kv_offsets[r + 1];
+    return k0 >= 0 && k1 >= k0 && k1 <= kv.kv_rows;
+  }
+  const long long P = kv.prefix_len[r];
+  if (P < 0 || P > (long long)kv.max_pages * kv.page_size) return false;
+  const int np = int((P + kv.page_size - 1) / kv.page_size);
+  const int32_t* row = kv.block_table + size_t(r) * size_t(kv.max_pages);
+  bool ok = true;
+  for (int e = 0; e < np; ++e) {
+    const int pg = row[e];
+    ok = ok && pg >= 0 && pg < kv.num_pages;
+  }
+  return ok;
 }
 
 struct RequestShape {
@@ -155,16 +183,21 @@ struct RequestShape {
 
 // A request's rows per head split into passes of at most 48 rows, as even as
 // possible; its hkv * passes streams form ceil(/4) groups over the same tiles.
-__device__ __forceinline__ RequestShape request_shape(const int32_t* q_offsets,
-                                                      const int64_t* kv_offsets,
-                                                      long long kv_rows, int max_rows, int R,
-                                                      int hkv, int G, int r) {
+// `ok` is request_ok of request r (evaluated once per plan).  A paged request's
+// kb is its index (its block table row), a contiguous one's its first row.
+__device__ __forceinline__ RequestShape request_shape(const int32_t* q_offsets, const KvSource& kv,
+                                                      bool ok, int R, int hkv, int G, int r) {
   RequestShape s = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-  if (r >= R || !request_ok(q_offsets, kv_offsets, kv_rows, max_rows, r)) return s;
+  if (r >= R || !ok) return s;
   s.q0 = q_offsets[r];
   s.nsl = q_offsets[r + 1] - s.q0;
-  s.kb = int(kv_offsets[r]);
-  s.P = int(kv_offsets[r + 1] - kv_offsets[r]);
+  if (kv.block_table == nullptr) {
+    s.kb = int(kv.kv_offsets[r]);
+    s.P = int(kv.kv_offsets[r + 1] - kv.kv_offsets[r]);
+  } else {
+    s.kb = r;
+    s.P = kv.prefix_len[r];
+  }
   const int rows = s.nsl * G;
   s.passes = (rows + kPassRows - 1) / kPassRows;
   if (s.passes == 0) return s;
@@ -176,20 +209,24 @@ __device__ __forceinline__ RequestShape request_shape(const int32_t* q_offsets,
 }
 
 __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
-    const int32_t* __restrict__ q_offsets, const int64_t* __restrict__ kv_offsets,
-    long long kv_rows, int R, int hkv, int G, int max_rows, int nb, long long ucap, AttnWs ws,
-    int32_t* status) {
+    const int32_t* __restrict__ q_offsets, KvSource kv, int R, int hkv, int G, int max_rows,
+    int nb, long long ucap, AttnWs ws, int32_t* status) {
   __shared__ int s_scan[kThreads / kWave + 1];
+  __shared__ uint8_t s_ok[ECHO_MAX_REQUESTS + 1];
   const int tid = threadIdx.x;
   int bits = 0;
-  for (int r = tid; r < R; r += kThreads)
-    if (!request_ok(q_offsets, kv_offsets, kv_rows, max_rows, r)) bits |= ECHO_DATA_BAD_OFFSETS;
+  for (int r = tid; r < R; r += kThreads) {
+    const bool ok = request_ok(q_offsets, kv, max_rows, r);
+    s_ok[r] = ok ? 1 : 0;
+    if (!ok) bits |= ECHO_DATA_BAD_OFFSETS;
+  }
+  __syncthreads();
+  auto ok_of = [&](int r) { return r < R && s_ok[r] != 0; };
 
   // pass A: total units and tiles
   long long T = 0, U = 0;
   for (int base = 0; base < R; base += kThreads) {
-    const RequestShape s =
-        request_shape(q_offsets, kv_offsets, kv_rows, max_rows, R, hkv, G, base + tid);
+    const RequestShape s = request_shape(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
     int tot_u, tot_t;
     block_exclusive_sum<kThreads>(s.groups, s_scan, &tot_u);
     block_exclusive_sum<kThreads>(s.groups * s.tiles, s_scan, &tot_t);
@@ -215,8 +252,7 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
   // pass B: units, the cut units and each workgroup's first unit
   int unit_run = 0, tile_run = 0, cut_run = 0;
   for (int base = 0; base < R; base += kThreads) {
-    const RequestShape s =
-        request_shape(q_offsets, kv_offsets, kv_rows, max_rows, R, hkv, G, base + tid);
+    const RequestShape s = request_shape(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
     int tot_u, tot_t;
     const int ub = unit_run + block_exclusive_sum<kThreads>(s.groups, s_scan, &tot_u);
     const int tb = tile_run + block_exclusive_sum<kThreads>(s.groups * s.tiles, s_scan, &tot_t);
@@ -542,6 +578,9 @@ struct MainArgs {
   const uint16_t* v_new;
   const uint16_t* k_cache;
   const uint16_t* v_cache;
+  const int32_t* block_table;  // paged prefix (else nullptr): see KvSource
+  int page_shift;              // log2 of the page size (>= 5: a tile never straddles pages)
+  int max_pages;
   const uint32_t* tree_mask;
   int W, hq, hkv, G;
   float scale2;
@@ -605,7 +644,16 @@ __device__ __forceinline__ void issue_next(Issuer& is, const MainArgs& a, const 
       tn = min(kTileKeys, is.ud.nslots - lt * kTileKeys);
     } else {
       const int pt = lt - is.ud.ntail;
-      const size_t row = size_t(is.ud.kb) + size_t(pt) * kTileKeys;
+      size_t row;
+      if (a.block_table == nullptr) {
+        row = size_t(is.ud.kb) + size_t(pt) * kTileKeys;
+      } else {
+        // wave-uniform index: a scalar load of the tile's page
+        const int pos = pt * kTileKeys;
+        const const_i32_t* bt = (const const_i32_t*)(a.block_table);
+        const int page = bt[size_t(is.ud.kb) * size_t(a.max_pages) + size_t(pos >> a.page_shift)];
+        row = (size_t(page) << a.page_shift) + size_t(pos & ((1 << a.page_shift) - 1));
+      }
       kb = a.k_cache + row * stride + sm.kvh * kD;
       vb = a.v_cache + row * stride + sm.kvh * kD;
       tn = min(kTileKeys, is.ud.P - pt * kTileKeys);
@@ -885,15 +933,27 @@ int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
   const size_t ucap = unit_capacity(a.R, a.max_rows, a.hq, a.hkv);
   AttnWs ws = attn_layout(a.workspace, ucap, nb);
   const int G = a.hq / a.hkv;
-  hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kThreads), 0, stream, a.q_offsets,
-                     a.kv_offsets, static_cast<long long>(a.kv_rows), a.R, a.hkv, G, a.max_rows,
-                     nb, static_cast<long long>(ucap), ws, a.status);
+  KvSource kv;
+  kv.kv_offsets = a.kv_offsets;
+  kv.kv_rows = static_cast<long long>(a.kv_rows);
+  kv.block_table = a.block_table;
+  kv.prefix_len = a.prefix_len;
+  kv.page_size = a.page_size;
+  kv.max_pages = a.max_pages;
+  kv.num_pages = static_cast<long long>(a.num_pages);
+  hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kThreads), 0, stream, a.q_offsets, kv, a.R,
+                     a.hkv, G, a.max_rows, nb, static_cast<long long>(ucap), ws, a.status);
   MainArgs m;
   m.q = a.q;
   m.k_new = a.k_new;
   m.v_new = a.v_new;
   m.k_cache = a.k_cache;
   m.v_cache = a.v_cache;
+  m.block_table = a.block_table;
+  m.page_shift = 0;
+  if (a.block_table != nullptr)
+    while ((1 << m.page_shift) < a.page_size) ++m.page_shift;
+  m.max_pages = a.max_pages;
   m.tree_mask = a.tree_mask;
   m.W = a.mask_words;
   m.hq = a.hq;
@@ -902,8 +962,9 @@ int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
   m.scale2 = a.sm_scale * kLog2e;
   m.out = a.out;
   m.lse = a.lse;
-  // the measurement events (if set) travel in the dispatch packet itself: no
-  // extra packets, no cache flushes between the launches
+  // the measurement events (if set) travel with the dispatch; they still leave a
+  // few microseconds of idle time around the kernel, so a step timed for
+  // throughput runs without them
   const bool prof = g_attn_ev_start != nullptr && g_attn_ev_stop != nullptr;
   void* main_args[] = {&m, &ws};
   if (hipExtLaunchKernel(reinterpret_cast<const void*>(&attn_main_kernel), dim3(unsigned(nb)),

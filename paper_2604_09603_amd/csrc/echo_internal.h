@@ -54,6 +54,15 @@ struct AttnArgs {
   const uint16_t* v_cache;
   const int64_t* kv_offsets;
   int64_t kv_rows;
+  // paged prefix (block_table != nullptr): request r's position p lives in page
+  // block_table[r * max_pages + p / page_size], row p % page_size, of
+  // k_cache / v_cache seen as [num_pages][page_size][Hkv][128]; its length is
+  // prefix_len[r] (kv_offsets and kv_rows are not used)
+  const int32_t* block_table;
+  const int32_t* prefix_len;
+  int32_t page_size;
+  int32_t max_pages;
+  int64_t num_pages;
   const int32_t* q_offsets;
   const uint32_t* tree_mask;
   int32_t mask_words;
@@ -75,6 +84,19 @@ int32_t launch_accept(const int32_t* q_offsets, const int32_t* slot_parent,
                       int32_t max_rows, int32_t max_depth, int32_t* accept_len,
                       int32_t* accept_slots, int32_t* bonus_token, int32_t* status,
                       hipStream_t stream);
+
+int32_t launch_accept_logits(const int32_t* q_offsets, const int32_t* slot_parent,
+                             const int32_t* slot_token, const uint16_t* logits, int64_t vocab,
+                             int32_t R, int32_t max_rows, int32_t max_depth, int32_t* target,
+                             int32_t* accept_len, int32_t* accept_slots, int32_t* bonus_token,
+                             int32_t* status, hipStream_t stream);
+
+int32_t launch_commit_kv(const int32_t* q_offsets, const int32_t* accept_len,
+                         const int32_t* accept_slots, int32_t max_depth, const uint16_t* k_new,
+                         const uint16_t* v_new, int32_t R, int32_t max_rows, int32_t hkv,
+                         uint16_t* k_pages, uint16_t* v_pages, int64_t num_pages,
+                         int32_t page_size, const int32_t* block_table, int32_t max_pages,
+                         int32_t* prefix_len, int32_t* status, hipStream_t stream);
 
 int device_cu_count();
 

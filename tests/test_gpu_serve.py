@@ -1,0 +1,256 @@
+"""GPU parity of the serving-step entry points: verification attention over a
+paged KV cache, target argmax + acceptance from logits, and the KV commit of
+the accepted path -- against the oracle (and the contiguous GPU path)."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests import gpu_common as gc
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu():
+    gc.require_gpu()
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_pages(k_cache, v_cache, kv_offsets, page_size, rng, spare=2):
+    """Scatter each request's prefix into shuffled pages; returns
+    (k_pages, v_pages, block_table, prefix_len)."""
+    R = len(kv_offsets) - 1
+    P = np.diff(kv_offsets).astype(np.int64)
+    npg = (P + page_size - 1) // page_size
+    maxp = int(npg.max()) + spare
+    total = int(npg.sum()) + spare * R
+    perm = rng.permutation(total).astype(np.int32)
+    hkv, D = k_cache.shape[1], k_cache.shape[2]
+    kp = np.zeros((total, page_size, hkv, D), np.uint16)
+    vp = np.zeros_like(kp)
+    bt = np.full((R, maxp), -1, np.int32)
+    k = 0
+    for r in range(R):
+        ids = perm[k:k + npg[r] + spare]
+        k += npg[r] + spare
+        bt[r, :len(ids)] = ids
+        n = int(npg[r])
+        if n:
+            pad = n * page_size
+            src = np.zeros((pad, hkv, D), np.uint16)
+            src[:P[r]] = k_cache[kv_offsets[r]:kv_offsets[r + 1]]
+            kp[ids[:n]] = src.reshape(n, page_size, hkv, D)
+            src[:P[r]] = v_cache[kv_offsets[r]:kv_offsets[r + 1]]
+            vp[ids[:n]] = src.reshape(n, page_size, hkv, D)
+    return kp, vp, bt, P.astype(np.int32)
+
+
+def _dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+
+
+def run_paged(b, m, kp, vp, bt, plen, page_size):
+    import torch
+    import paper_2604_09603_amd as pkg
+    from paper_2604_09603_amd.step import _aligned_workspace
+    cfg = b["cfg"]
+    cap = cfg.R + cfg.budget
+    i16 = lambda a: _dev(np.asarray(a, np.uint16).view(np.int16))
+    out = torch.full((cap, cfg.hq, 128), float("nan"), dtype=torch.float32, device="cuda:0")
+    lse = torch.full((cap, cfg.hq), float("nan"), dtype=torch.float32, device="cuda:0")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda:0")
+    ws = _aligned_workspace(pkg.tree_verify_attn_workspace_size(cfg.R, cap, cfg.hq, cfg.hkv),
+                            "cuda:0")
+    pkg.echo_tree_verify_attn_paged(i16(b["q"]), i16(b["k_new"]), i16(b["v_new"]), i16(kp),
+                                    i16(vp), page_size, _dev(bt), _dev(plen),
+                                    _dev(m["q_offsets"].astype(np.int32)),
+                                    _dev(m["tree_mask"].view(np.int32)), cfg.mask_words, cfg.R,
+                                    cap, cfg.hq, cfg.hkv, 128, float(b["sm_scale"]), out, lse, ws,
+                                    status=status)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), lse.cpu().numpy(), int(status.item())
+
+
+@pytest.mark.parametrize("name,page_size", [("tiny", 32), ("tiny", 256), ("l8b", 64),
+                                            ("l70b", 128), ("q235b", 64), ("long", 256)])
+def test_paged_attention_matches_contiguous(name, page_size):
+    """Same result as the contiguous GPU path (bit for bit: same tiles in the same
+    order) and within tolerance of the oracle."""
+    b = synth.make_batch(name, 0)
+    ref = gc.oracle_front(b)
+    m = ref["mask"]
+    rng = np.random.default_rng(page_size)
+    _log(f"[serve] paged {name} page_size={page_size}: building pages")
+    kp, vp, bt, plen = to_pages(b["k_cache"], b["v_cache"], b["kv_offsets"], page_size, rng)
+    _log(f"[serve] paged {name}: gpu")
+    out, lse, status = run_paged(b, m, kp, vp, bt, plen, page_size)
+    assert status == 0
+    st, res = gc.run_gpu(b, ref["target"])
+    nq = m["num_slots"]
+    assert np.array_equal(out[:nq].view(np.uint32), res["out"][:nq].view(np.uint32))
+    assert np.array_equal(lse[:nq].view(np.uint32), res["lse"][:nq].view(np.uint32))
+    assert np.all(np.isnan(out[nq:]))
+    rows = list(range(nq)) if name == "tiny" else gc.sample_rows(m["q_offsets"], rng)
+    cfg = b["cfg"]
+    ro, rl, _ = oracle.tree_verify_attn_paged(b["q"], b["k_new"], b["v_new"], kp, vp, bt, plen,
+                                              page_size, m["q_offsets"], m["tree_mask"], cfg.hq,
+                                              cfg.hkv, b["sm_scale"], rows=rows)
+    gc.compare_attn(out, lse, ro, rl, rows)
+
+
+def test_paged_attention_missing_page_skips_the_request():
+    b = synth.make_batch("tiny", 3)
+    ref = gc.oracle_front(b)
+    m = ref["mask"]
+    kp, vp, bt, plen = to_pages(b["k_cache"], b["v_cache"], b["kv_offsets"], 64,
+                                np.random.default_rng(1))
+    bt[2, 1] = -1                                    # request 2 loses its second page
+    out, lse, status = run_paged(b, m, kp, vp, bt, plen, 64)
+    assert status & oracle.status.BAD_OFFSETS
+    q0, q1 = int(m["q_offsets"][2]), int(m["q_offsets"][3])
+    assert np.all(np.isnan(out[q0:q1]))
+    cfg = b["cfg"]
+    rows = [s for s in range(m["num_slots"]) if not q0 <= s < q1]
+    ro, rl, _ = oracle.tree_verify_attn_paged(b["q"], b["k_new"], b["v_new"], kp, vp, bt, plen,
+                                              64, m["q_offsets"], m["tree_mask"], cfg.hq, cfg.hkv,
+                                              b["sm_scale"], rows=rows)
+    gc.compare_attn(out, lse, ro, rl, rows)
+
+
+def _accept_logits_case(b, m, vocab, rng, ties=True, nan_rows=0):
+    import torch
+    import paper_2604_09603_amd as pkg
+    cfg = b["cfg"]
+    cap = cfg.R + cfg.budget
+    nq = m["num_slots"]
+    if ties:   # few distinct values: ties are everywhere
+        vals = torch.randint(-6, 6, (cap, vocab), dtype=torch.int32, device="cuda:0")
+        logits = (vals.float() * 0.5).to(torch.bfloat16)
+    else:
+        logits = (torch.randn(cap, vocab, device="cuda:0") * 3).to(torch.bfloat16)
+    for i in range(nan_rows):
+        logits[i * 3, ::7] = float("nan")
+        if i == 0:
+            logits[0, :] = float("nan")
+    lg = logits.view(torch.int16)
+    d = lambda a: _dev(np.asarray(a, np.int32))
+    tgt = torch.full((cap,), -7, dtype=torch.int32, device="cuda:0")
+    al = torch.zeros(cfg.R, dtype=torch.int32, device="cuda:0")
+    aslots = torch.zeros((cfg.R, 16), dtype=torch.int32, device="cuda:0")
+    bonus = torch.zeros(cfg.R, dtype=torch.int32, device="cuda:0")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda:0")
+    pkg.echo_accept_logits(d(m["q_offsets"]), d(m["slot_parent"]), d(m["slot_token"]), lg, cfg.R,
+                           cap, 16, tgt, al, aslots, bonus, status=status)
+    torch.cuda.synchronize()
+    host_logits = lg.cpu().numpy().view(np.uint16)
+    want = oracle.accept_from_logits(m["q_offsets"], m["slot_parent"], m["slot_token"],
+                                     host_logits, 16)
+    t = tgt.cpu().numpy()
+    assert np.array_equal(t[:nq], want["target_token"]), "argmax differs"
+    assert np.all(t[nq:] == -7)
+    assert np.array_equal(al.cpu().numpy(), want["accept_len"])
+    assert np.array_equal(aslots.cpu().numpy(), want["accept_slots"])
+    assert np.array_equal(bonus.cpu().numpy(), want["bonus_token"])
+    assert int(status.item()) == want["status"]
+
+
+@pytest.mark.parametrize("name,vocab,ties", [("tiny", 32, True), ("tiny", 1001, True),
+                                             ("l8b", 128256, False), ("q235b", 151936, True),
+                                             ("q235b", 151937, False)])
+def test_accept_from_logits(name, vocab, ties):
+    b = synth.make_batch(name, 1)
+    ref = gc.oracle_front(b)
+    _log(f"[serve] accept_logits {name} V={vocab} ties={ties}")
+    _accept_logits_case(b, ref["mask"], vocab, np.random.default_rng(0), ties=ties,
+                        nan_rows=2 if name == "tiny" else 0)
+
+
+def test_commit_kv_matches_oracle():
+    import torch
+    import paper_2604_09603_amd as pkg
+    b = synth.make_batch("l8b", 2)
+    ref = gc.oracle_front(b)
+    m, a = ref["mask"], ref["accept"]
+    cfg = b["cfg"]
+    cap = cfg.R + cfg.budget
+    rng = np.random.default_rng(4)
+    page_size = 16
+    kp, vp, bt, plen = to_pages(b["k_cache"], b["v_cache"], b["kv_offsets"], page_size, rng,
+                                spare=3)
+    bt[5, :] = -1                                     # request 5 has no pages: refused
+    d32 = lambda x: _dev(np.asarray(x, np.int32))
+    i16 = lambda x: _dev(np.asarray(x, np.uint16).view(np.int16))
+    kpd, vpd, pld = i16(kp), i16(vp), d32(plen)
+    status = torch.zeros(1, dtype=torch.int32, device="cuda:0")
+    pkg.echo_commit_kv(d32(m["q_offsets"]), d32(a["accept_len"]), d32(a["accept_slots"]), 16,
+                       i16(b["k_new"]), i16(b["v_new"]), cfg.R, cap, cfg.hkv, kpd, vpd,
+                       page_size, d32(bt), pld, status=status)
+    torch.cuda.synchronize()
+    kp2, vp2, P2, s = oracle.commit_kv(m["q_offsets"], a["accept_len"], a["accept_slots"],
+                                       b["k_new"], b["v_new"], kp, vp, bt, plen, page_size)
+    assert np.array_equal(pld.cpu().numpy(), P2)
+    assert np.array_equal(kpd.cpu().numpy().view(np.uint16), kp2)
+    assert np.array_equal(vpd.cpu().numpy().view(np.uint16), vp2)
+    assert int(status.item()) == s == oracle.status.BAD_OFFSETS
+
+
+def test_serving_step_with_paged_cache():
+    """gate -> mask -> paged attention -> accept from logits -> commit, then a
+    second verification over the grown cache, on the tiny preset."""
+    import torch
+    import paper_2604_09603_amd as pkg
+    from paper_2604_09603_amd.step import VerifyStep, _aligned_workspace
+    b = synth.make_batch("tiny", 4)
+    cfg = b["cfg"]
+    cap = cfg.R + cfg.budget
+    rng = np.random.default_rng(6)
+    page_size = 32
+    kp, vp, bt, plen = to_pages(b["k_cache"], b["v_cache"], b["kv_offsets"], page_size, rng,
+                                spare=2)
+    st = VerifyStep(b)
+    st.gate()
+    st.mask()
+    res = st.fetch()
+    ref = gc.oracle_front(b)
+    m = ref["mask"]
+    out, lse, status = run_paged(b, m, kp, vp, bt, plen, page_size)
+    assert status == 0
+    logits = (torch.randn(cap, 32, device="cuda:0") * 2).to(torch.bfloat16).view(torch.int16)
+    d32 = lambda x: _dev(np.asarray(x, np.int32))
+    i16 = lambda x: _dev(np.asarray(x, np.uint16).view(np.int16))
+    tgt = torch.zeros(cap, dtype=torch.int32, device="cuda:0")
+    pkg.echo_accept_logits(st.q_offsets, st.slot_parent, st.slot_token, logits, cfg.R, cap, 16,
+                           tgt, st.accept_len, st.accept_slots, st.bonus_token, status=st.status)
+    kpd, vpd, pld, btd = i16(kp), i16(vp), d32(plen), d32(bt)
+    pkg.echo_commit_kv(st.q_offsets, st.accept_len, st.accept_slots, 16, st.k_new, st.v_new,
+                       cfg.R, cap, cfg.hkv, kpd, vpd, page_size, btd, pld, status=st.status)
+    torch.cuda.synchronize()
+    hl = logits.cpu().numpy().view(np.uint16)
+    acc = oracle.accept_from_logits(m["q_offsets"], m["slot_parent"], m["slot_token"], hl, 16)
+    kp2, vp2, P2, s = oracle.commit_kv(m["q_offsets"], acc["accept_len"], acc["accept_slots"],
+                                       b["k_new"], b["v_new"], kp, vp, bt, plen, page_size)
+    assert s == 0 and int(st.status.item()) == 0
+    assert np.array_equal(st.accept_len.cpu().numpy(), acc["accept_len"])
+    assert np.array_equal(pld.cpu().numpy(), P2)
+    assert np.array_equal(kpd.cpu().numpy().view(np.uint16), kp2)
+    # next step: every request verifies one new root over the grown prefix
+    q1 = np.asarray(b["q"][:cfg.R])
+    qo1 = np.arange(cfg.R + 1, dtype=np.int32)
+    mask1 = np.zeros((cap, cfg.mask_words), np.uint32)
+    mask1[:cfg.R, 0] = 1
+    b2 = dict(b, q=np.concatenate([q1, np.zeros((cfg.budget,) + q1.shape[1:], np.uint16)]))
+    out2, lse2, st2 = run_paged(b2, dict(q_offsets=qo1, tree_mask=mask1), kp2, vp2, bt, P2,
+                                page_size)
+    assert st2 == 0
+    ro, rl, _ = oracle.tree_verify_attn_paged(b2["q"], b["k_new"], b["v_new"], kp2, vp2, bt, P2,
+                                              page_size, qo1, mask1, cfg.hq, cfg.hkv,
+                                              b["sm_scale"])
+    gc.compare_attn(out2, lse2, ro, rl, range(cfg.R))
