@@ -151,6 +151,15 @@ def main():
                     help="gate stage: global top-B (default), checkpoint gating before it, or "
                          "Alg. 1's elastic scheduler (checkpoints at depths 1, 3, 5, W_topk = 2, "
                          "W_max = the drafted branching)")
+    ap.add_argument("--page-size", type=int, default=0,
+                    help="read the KV prefixes from a paged cache with pages of this many rows "
+                         "(echo_tree_verify_attn_paged); 0 = contiguous")
+    ap.add_argument("--serve", action="store_true",
+                    help="the serving step: paged cache (64-row pages unless --page-size), "
+                         "acceptance from bf16 target logits (echo_accept_logits) and the KV "
+                         "commit of the accepted path (echo_commit_kv)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step in a HIP graph and time graph replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES, five times (the "
                          "reference kernel that scales the HBM byte counters)")
@@ -189,19 +198,47 @@ def main():
         elastic = (2, cfg.branch)
     else:
         checkpoints = gate_checkpoints(args.gate_policy, args.config, cfg.depth)
-    st = VerifyStep(batch, device="cuda:0", checkpoints=checkpoints, elastic=elastic)
+    page_size = args.page_size or (64 if args.serve else 0)
+    st = VerifyStep(batch, device="cuda:0", checkpoints=checkpoints, elastic=elastic,
+                    page_size=page_size or None, serve=args.serve)
     # the target model's argmax per slot is a stand-in input: gather it once for this batch
     st.gate()
     st.mask()
     torch.cuda.synchronize()
     res0 = st.fetch()
-    st.set_target(synth.target_for_slots(batch, res0["q_offsets"], res0["slot_cand"]))
+    tgt = synth.target_for_slots(batch, res0["q_offsets"], res0["slot_cand"])
+    st.set_target(tgt)
+    if args.serve:
+        # synthetic target logits whose argmax is the stand-in target of each slot
+        gen = torch.Generator(device="cuda:0")
+        gen.manual_seed(args.seed)
+        logits = torch.randn((st.cap, cfg.vocab), generator=gen, device="cuda:0")
+        rows = torch.arange(len(tgt), device="cuda:0")
+        logits[rows, torch.from_numpy(tgt.astype(np.int64)).to("cuda:0")] = 8.0
+        st.set_logits(logits.to(torch.bfloat16))
+        del logits
     torch.cuda.synchronize()
 
     log(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):
         st.run()
     torch.cuda.synchronize()
+    step_fn = st.run
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            st.run()                      # a warm launch on the capture stream
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            st.run()
+        torch.cuda.synchronize()
+        step_fn = graph.replay
+        for _ in range(3):
+            step_fn()
+        torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
     # 1. the timed steps: the whole step, nothing else on the stream
@@ -212,7 +249,7 @@ def main():
     wall0 = time.perf_counter()
     t_start.record(stream)
     for _ in range(args.steps):
-        st.run()
+        step_fn()
     t_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -268,6 +305,8 @@ def main():
             "kv_prefix_tokens": int(batch["kv_offsets"][-1]), "seed": args.seed,
             "parallelism": "single GPU", "gate_policy": args.gate_policy,
             "checkpoints": checkpoints, "elastic_widths": elastic,
+            "kv_layout": f"paged, {page_size}-row pages" if page_size else "contiguous",
+            "serve_step": bool(args.serve), "hip_graph": bool(args.graph),
         },
         "roofline": {
             "kernel": "attn_main_kernel",

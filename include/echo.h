@@ -250,7 +250,8 @@ size_t echo_tree_verify_attn_workspace_size(int32_t R, int32_t max_rows, int32_t
  * A request whose prefix needs a page id outside [0, num_pages) (or a length
  * beyond its block-table row) is skipped with ECHO_DATA_BAD_OFFSETS, like an
  * invalid kv_offsets range.  Everything else is as for echo_tree_verify_attn,
- * including the workspace size.
+ * including the workspace size (ECHO_ERR_UNSUPPORTED in the unlikely case that
+ * R * ceil(max_pages_per_request / 256) page-check flags do not fit in it).
  */
 int32_t echo_tree_verify_attn_paged(
     const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new, const uint16_t* k_pages,

@@ -153,10 +153,14 @@ struct KvSource {
   int page_size;
   int max_pages;
   long long num_pages;
+  const int32_t* page_bad;  // [R][page_chunks]: written by attn_pages, read by the plan
+  int page_chunks;
 };
 
-// Slot range and prefix of request r are usable (every page of a paged prefix
-// present and in range).
+constexpr int kPageChunk = 256;  // page ids checked per attn_pages workgroup
+
+// Slot range and prefix extent of request r are usable (for a paged prefix:
+// its length fits its block-table row; the page ids are checked separately).
 __device__ __forceinline__ bool request_ok(const int32_t* q_offsets, const KvSource& kv,
                                            int max_rows, int r) {
   const int q0 = q_offsets[r], q1 = q_offsets[r + 1];
@@ -166,15 +170,25 @@ __device__ __forceinline__ bool request_ok(const int32_t* q_offsets, const KvSou
     return k0 >= 0 && k1 >= k0 && k1 <= kv.kv_rows;
   }
   const long long P = kv.prefix_len[r];
-  if (P < 0 || P > (long long)kv.max_pages * kv.page_size) return false;
-  const int np = int((P + kv.page_size - 1) / kv.page_size);
-  const int32_t* row = kv.block_table + size_t(r) * size_t(kv.max_pages);
-  bool ok = true;
-  for (int e = 0; e < np; ++e) {
-    const int pg = row[e];
-    ok = ok && pg >= 0 && pg < kv.num_pages;
+  return P >= 0 && P <= (long long)kv.max_pages * kv.page_size;
+}
+
+// Paged prefixes: workgroup (r, c) checks page ids c * 256 .. c * 256 + 255 of
+// request r and records whether one is outside [0, num_pages) (every chunk is
+// written, so nothing needs clearing first).
+__global__ __launch_bounds__(kPageChunk) void attn_pages_kernel(KvSource kv) {
+  const int r = blockIdx.x, c = blockIdx.y;
+  const long long P = kv.prefix_len[r];
+  const bool len_ok = P >= 0 && P <= (long long)kv.max_pages * kv.page_size;
+  const long long np = len_ok ? (P + kv.page_size - 1) / kv.page_size : 0;
+  const long long e = (long long)c * kPageChunk + threadIdx.x;
+  int bad = 0;
+  if (e < np) {
+    const int pg = kv.block_table[size_t(r) * size_t(kv.max_pages) + size_t(e)];
+    bad = pg < 0 || pg >= kv.num_pages;
   }
-  return ok;
+  bad = __syncthreads_or(bad);
+  if (threadIdx.x == 0) const_cast<int32_t*>(kv.page_bad)[size_t(r) * kv.page_chunks + c] = bad;
 }
 
 struct RequestShape {
@@ -216,7 +230,9 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
   const int tid = threadIdx.x;
   int bits = 0;
   for (int r = tid; r < R; r += kThreads) {
-    const bool ok = request_ok(q_offsets, kv, max_rows, r);
+    bool ok = request_ok(q_offsets, kv, max_rows, r);
+    if (kv.block_table != nullptr)
+      for (int c = 0; c < kv.page_chunks; ++c) ok = ok && kv.page_bad[size_t(r) * kv.page_chunks + c] == 0;
     s_ok[r] = ok ? 1 : 0;
     if (!ok) bits |= ECHO_DATA_BAD_OFFSETS;
   }
@@ -941,6 +957,17 @@ int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
   kv.page_size = a.page_size;
   kv.max_pages = a.max_pages;
   kv.num_pages = static_cast<long long>(a.num_pages);
+  kv.page_bad = nullptr;
+  kv.page_chunks = 0;
+  if (a.block_table != nullptr) {
+    // the flags borrow the start of the partials, which the main kernel only
+    // writes later on the same stream
+    kv.page_chunks = (a.max_pages + kPageChunk - 1) / kPageChunk;
+    if (size_t(a.R) * size_t(kv.page_chunks) * 4 > part_rows(nb) * kD * 4) return ECHO_ERR_UNSUPPORTED;
+    kv.page_bad = reinterpret_cast<const int32_t*>(ws.part_o);
+    hipLaunchKernelGGL(attn_pages_kernel, dim3(unsigned(a.R), unsigned(kv.page_chunks)),
+                       dim3(kPageChunk), 0, stream, kv);
+  }
   hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kThreads), 0, stream, a.q_offsets, kv, a.R,
                      a.hkv, G, a.max_rows, nb, static_cast<long long>(ucap), ws, a.status);
   MainArgs m;

@@ -3,10 +3,11 @@
 // the commit of each request's accepted path into a paged KV cache.
 //
 //   target_argmax   one workgroup per slot row: streams the row's bfloat16
-//                   logits with 16-byte loads (HBM-bound: Nq * V * 2 bytes) and
-//                   keeps, per thread, the first largest value in its own index
-//                   order; a workgroup reduction picks the largest value, ties
-//                   to the smaller token id.  Then the acceptance kernel.
+//                   logits with 16-byte loads, eight in flight per thread
+//                   (HBM-bound: Nq * V * 2 bytes), keeps per thread the first
+//                   largest value in its own index order; a workgroup reduction
+//                   picks the largest value, ties to the smaller token id.  Then
+//                   the acceptance kernel.
 //   commit_kv       one workgroup per request: copies the root slot's and the
 //                   accepted slots' K and V rows into their pages, then advances
 //                   the request's cached length.
@@ -16,84 +17,116 @@
 namespace echo {
 namespace {
 
-constexpr int kArgThreads = 256;
+constexpr int kArgThreads = 512;  // two workgroups per CU: every slot row of a batch is resident
+constexpr int kArgUnroll = 8;  // 16-byte loads in flight per thread
 constexpr int kCommitThreads = 256;
+constexpr uint32_t kNoIdx = 0xFFFFFFFFu;
 
-// Orderable 16-bit key of a bfloat16 value: larger value -> larger key,
-// -0 == +0, every NaN -> 0 (below -inf, whose key is 0x007F).
-__device__ __forceinline__ uint32_t bf16_key(uint32_t h) {
-  h &= 0xFFFFu;
-  if ((h & 0x7FFFu) > 0x7F80u) return 0u;  // NaN
-  if (h == 0x8000u) h = 0u;                // -0 -> +0
-  return (h & 0x8000u) ? (~h & 0xFFFFu) : (h | 0x8000u);
-}
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// (key, index) -> a word whose order is (key descending, index ascending)
-__device__ __forceinline__ uint64_t arg_word(uint32_t key, uint32_t idx) {
-  return (uint64_t(key) << 32) | uint64_t(0xFFFFFFFFu - idx);
-}
-
+// One workgroup per slot row.  Each thread keeps the first strictly largest
+// value of its own elements, visited in increasing index order (a NaN never
+// compares greater, so it is never kept; -0 and +0 compare equal); the
+// workgroup then takes the largest value, ties to the smaller index.  A row
+// in which nothing beats -inf (only -inf and NaN) is resolved by a second
+// scan for its first -inf (a row of NaN only gives 0).
 __global__ __launch_bounds__(kArgThreads) void target_argmax_kernel(
     const uint16_t* __restrict__ logits, long long vocab, const int32_t* __restrict__ q_offsets,
     int R, int32_t* __restrict__ target) {
-  __shared__ uint64_t s_best[kArgThreads / kWave];
+  __shared__ float s_val[kArgThreads / kWave];
+  __shared__ uint32_t s_idx[kArgThreads / kWave];
+  __shared__ uint32_t s_first_inf;
   const int s = blockIdx.x;
   const int nq = q_offsets[R];
   if (s >= nq) return;  // uniform over the workgroup
   const uint16_t* row = logits + size_t(s) * size_t(vocab);
   const int tid = threadIdx.x;
-  uint64_t best = 0ull;  // below every real (key, index)
+  float best = -__builtin_inff();
+  uint32_t bidx = kNoIdx;
+  auto take = [&](float v, uint32_t i) {
+    if (v > best) {
+      best = v;
+      bidx = i;
+    }
+  };
   // scalar head up to 16-byte alignment, 8-value body, scalar tail
   const long long head =
       min<long long>(vocab, ((16 - (reinterpret_cast<uintptr_t>(row) & 15)) & 15) / 2);
   const long long nvec = (vocab - head) / 8;
   const long long tail0 = head + nvec * 8;
-  auto take = [&](uint32_t h, long long v) {
-    const uint64_t w = arg_word(bf16_key(h), uint32_t(v));
-    best = w > best ? w : best;
-  };
-  for (long long v = tid; v < head; v += kArgThreads) take(row[v], v);
+  // the head precedes the body in index order: its elements are taken first
+  for (long long v = tid; v < head; v += kArgThreads)
+    take(__uint_as_float(uint32_t(row[v]) << 16), uint32_t(v));
   const uint4* body = reinterpret_cast<const uint4*>(row + head);
   long long c = tid;
-  for (; c + 3 * kArgThreads < nvec; c += 4 * kArgThreads) {
-    uint4 x[4];
+  for (; c + (kArgUnroll - 1) * kArgThreads < nvec; c += kArgUnroll * kArgThreads) {
+    uint4 x[kArgUnroll];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) x[u] = body[c + u * kArgThreads];
+    for (int u = 0; u < kArgUnroll; ++u) x[u] = body[c + u * kArgThreads];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const long long v0 = head + (c + u * kArgThreads) * 8;
-      const uint32_t w4[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        take(w4[e] & 0xFFFFu, v0 + 2 * e);
-        take(w4[e] >> 16, v0 + 2 * e + 1);
-      }
+    for (int u = 0; u < kArgUnroll; ++u) {
+      const uint32_t v0 = uint32_t(head + (c + u * kArgThreads) * 8);
+      take(bf16_lo(x[u].x), v0 + 0);
+      take(bf16_hi(x[u].x), v0 + 1);
+      take(bf16_lo(x[u].y), v0 + 2);
+      take(bf16_hi(x[u].y), v0 + 3);
+      take(bf16_lo(x[u].z), v0 + 4);
+      take(bf16_hi(x[u].z), v0 + 5);
+      take(bf16_lo(x[u].w), v0 + 6);
+      take(bf16_hi(x[u].w), v0 + 7);
     }
   }
   for (; c < nvec; c += kArgThreads) {
     const uint4 x = body[c];
-    const long long v0 = head + c * 8;
-    const uint32_t w4[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      take(w4[e] & 0xFFFFu, v0 + 2 * e);
-      take(w4[e] >> 16, v0 + 2 * e + 1);
-    }
+    const uint32_t v0 = uint32_t(head + c * 8);
+    take(bf16_lo(x.x), v0 + 0);
+    take(bf16_hi(x.x), v0 + 1);
+    take(bf16_lo(x.y), v0 + 2);
+    take(bf16_hi(x.y), v0 + 3);
+    take(bf16_lo(x.z), v0 + 4);
+    take(bf16_hi(x.z), v0 + 5);
+    take(bf16_lo(x.w), v0 + 6);
+    take(bf16_hi(x.w), v0 + 7);
   }
-  for (long long v = tail0 + tid; v < vocab; v += kArgThreads) take(row[v], v);
-  // workgroup maximum of the words
+  // the tail follows every body element in index order
+  for (long long v = tail0 + tid; v < vocab; v += kArgThreads)
+    take(__uint_as_float(uint32_t(row[v]) << 16), uint32_t(v));
+  // workgroup: largest value, ties (and -0 == +0) to the smaller index
+  auto better = [](float va, uint32_t ia, float vb, uint32_t ib) {
+    if (ib == kNoIdx) return false;
+    if (ia == kNoIdx) return true;
+    return vb > va || (vb == va && ib < ia);
+  };
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
-    const uint64_t o = __shfl_xor(best, off, kWave);
-    best = o > best ? o : best;
+    const float ov = __shfl_xor(best, off, kWave);
+    const uint32_t oi = uint32_t(__shfl_xor(int(bidx), off, kWave));
+    if (better(best, bidx, ov, oi)) {
+      best = ov;
+      bidx = oi;
+    }
   }
-  if ((tid & (kWave - 1)) == 0) s_best[tid / kWave] = best;
+  if ((tid & (kWave - 1)) == 0) {
+    s_val[tid / kWave] = best;
+    s_idx[tid / kWave] = bidx;
+  }
+  if (tid == 0) s_first_inf = kNoIdx;
   __syncthreads();
-  if (tid == 0) {
-    uint64_t b = s_best[0];
-    for (int w = 1; w < kArgThreads / kWave; ++w) b = s_best[w] > b ? s_best[w] : b;
-    target[s] = int32_t(0xFFFFFFFFu - uint32_t(b));
+  float bv = s_val[0];
+  uint32_t bi = s_idx[0];
+  for (int w = 1; w < kArgThreads / kWave; ++w)
+    if (better(bv, bi, s_val[w], s_idx[w])) {
+      bv = s_val[w];
+      bi = s_idx[w];
+    }
+  if (bi == kNoIdx) {  // nothing above -inf: the first -inf, else 0
+    for (long long v = tid; v < vocab; v += kArgThreads)
+      if (row[v] == 0xFF80u) atomicMin(&s_first_inf, uint32_t(v));
+    __syncthreads();
+    bi = s_first_inf == kNoIdx ? 0u : s_first_inf;
   }
+  if (tid == 0) target[s] = int32_t(bi);
 }
 
 __global__ __launch_bounds__(kCommitThreads) void commit_kv_kernel(

@@ -9,9 +9,10 @@ caller supplies it (``set_target``) because it comes from the target model.
 import numpy as np
 import torch
 
-from . import (HEAD_DIM, MAX_DEPTH, echo_accept, echo_build_tree_mask, echo_gate,
-               echo_gate_elastic, echo_gate_sparse, echo_tree_verify_attn,
-               gate_elastic_workspace_size, gate_workspace_size, tree_verify_attn_workspace_size)
+from . import (HEAD_DIM, MAX_DEPTH, echo_accept, echo_accept_logits, echo_build_tree_mask,
+               echo_commit_kv, echo_gate, echo_gate_elastic, echo_gate_sparse,
+               echo_tree_verify_attn, echo_tree_verify_attn_paged, gate_elastic_workspace_size,
+               gate_workspace_size, tree_verify_attn_workspace_size)
 
 
 def _aligned_workspace(nbytes, device):
@@ -31,10 +32,16 @@ class VerifyStep:
     """``checkpoints``: optional sequence of (depth, ln tau) pairs; when given the
     gate stage is echo_gate_sparse (checkpoint truncation, then top-B).
     ``elastic``: optional (w_topk, w_max); when given the gate stage is
-    echo_gate_elastic (Alg. 1) with the checkpoints (none if not given)."""
+    echo_gate_elastic (Alg. 1) with the checkpoints (none if not given).
+    ``page_size``: optional; the KV prefixes are then scattered over shuffled
+    pages of that many rows (with room for the commits of one step) and the
+    attention stage is echo_tree_verify_attn_paged.
+    ``serve``: with ``page_size``, acceptance reads the target argmax from
+    logits (``set_logits``) and each step ends with echo_commit_kv; the cached
+    lengths are restored afterwards so that every step repeats the same work."""
 
     def __init__(self, batch, device="cuda:0", max_depth=MAX_DEPTH, checkpoints=None,
-                 elastic=None):
+                 elastic=None, page_size=None, serve=False, page_seed=0):
         cfg = batch["cfg"]
         self.checkpoints = None if checkpoints is None else [(int(d), float(t))
                                                              for d, t in checkpoints]
@@ -65,6 +72,12 @@ class VerifyStep:
         self.k_cache = i16(batch["k_cache"])
         self.v_cache = i16(batch["v_cache"])
         self.sm_scale = float(batch["sm_scale"])
+        self.page_size = None if page_size is None else int(page_size)
+        self.serve = bool(serve)
+        if self.serve and self.page_size is None:
+            raise ValueError("the serving step needs a paged cache (page_size)")
+        if self.page_size is not None:
+            self._make_pages(batch, page_seed)
         # outputs
         z32 = lambda *s: torch.zeros(s, dtype=torch.int32, device=d)
         self.path_score = torch.zeros(max(self.N, 1), dtype=torch.float32, device=d)
@@ -88,6 +101,40 @@ class VerifyStep:
         self.gate_ws = _aligned_workspace(ws_size(self.R, self.N, self.B), d)
         self.attn_ws = _aligned_workspace(
             tree_verify_attn_workspace_size(self.R, self.cap, self.hq, self.hkv, self.D), d)
+
+    def _make_pages(self, batch, seed):
+        """Scatter every prefix over shuffled pages; each request also gets the
+        pages its commit of one step (at most 1 + max_depth rows) can reach."""
+        S = self.page_size
+        P = np.asarray(batch["prefix_len"], np.int64)
+        kvo = np.asarray(batch["kv_offsets"], np.int64)
+        npg = (P + 1 + self.max_depth + S - 1) // S
+        total = int(npg.sum())
+        perm = np.random.default_rng(seed).permutation(total).astype(np.int64)
+        bt = np.full((self.R, int(npg.max())), -1, np.int32)
+        dest = np.empty(int(kvo[-1]), np.int64)
+        k = 0
+        for r in range(self.R):
+            ids = perm[k:k + npg[r]]
+            k += npg[r]
+            bt[r, :npg[r]] = ids
+            pos = np.arange(P[r])
+            dest[kvo[r]:kvo[r + 1]] = ids[pos // S] * S + pos % S
+        d = self.device
+        shape = (total, S, self.hkv, self.D)
+        self.k_pages = torch.zeros(shape, dtype=torch.int16, device=d)
+        self.v_pages = torch.zeros(shape, dtype=torch.int16, device=d)
+        idx = torch.from_numpy(dest).to(d)
+        self.k_pages.view(total * S, self.hkv, self.D)[idx] = self.k_cache
+        self.v_pages.view(total * S, self.hkv, self.D)[idx] = self.v_cache
+        self.block_table = _dev(bt, d)
+        self.cached_len = self.prefix_len.clone()   # grows with commits
+        self.logits = None
+        self.target_out = torch.zeros(self.cap, dtype=torch.int32, device=d)
+
+    def set_logits(self, logits):
+        """bf16 target logits [cap, V] (torch.bfloat16 or int16 bits) on the device."""
+        self.logits = logits.view(torch.int16) if logits.dtype == torch.bfloat16 else logits
 
     # ---- the four stages -------------------------------------------------
     def gate(self, stream=None):
@@ -116,6 +163,13 @@ class VerifyStep:
                              stream=stream)
 
     def attn(self, stream=None):
+        if self.page_size is not None:
+            echo_tree_verify_attn_paged(self.q, self.k_new, self.v_new, self.k_pages, self.v_pages,
+                                        self.page_size, self.block_table, self.cached_len,
+                                        self.q_offsets, self.tree_mask, self.W, self.R, self.cap,
+                                        self.hq, self.hkv, self.D, self.sm_scale, self.out,
+                                        self.lse, self.attn_ws, status=self.status, stream=stream)
+            return
         echo_tree_verify_attn(self.q, self.k_new, self.v_new, self.k_cache, self.v_cache,
                               self.kv_offsets, self.kv_rows, self.q_offsets, self.tree_mask,
                               self.W, self.R, self.cap, self.hq, self.hkv, self.D, self.sm_scale,
@@ -123,15 +177,32 @@ class VerifyStep:
                               stream=stream)
 
     def accept(self, stream=None):
+        if self.serve:
+            echo_accept_logits(self.q_offsets, self.slot_parent, self.slot_token, self.logits,
+                               self.R, self.cap, self.max_depth, self.target_out,
+                               self.accept_len, self.accept_slots, self.bonus_token,
+                               status=self.status, stream=stream)
+            return
         echo_accept(self.q_offsets, self.slot_parent, self.slot_token, self.target_token, self.R,
                     self.cap, self.max_depth, self.accept_len, self.accept_slots,
                     self.bonus_token, status=self.status, stream=stream)
+
+    def commit(self, stream=None):
+        echo_commit_kv(self.q_offsets, self.accept_len, self.accept_slots, self.max_depth,
+                       self.k_new, self.v_new, self.R, self.cap, self.hkv, self.k_pages,
+                       self.v_pages, self.page_size, self.block_table, self.cached_len,
+                       status=self.status, stream=stream)
 
     def run(self, stream=None):
         self.gate(stream)
         self.mask(stream)
         self.attn(stream)
         self.accept(stream)
+        if self.serve:
+            self.commit(stream)
+            # the next step repeats this one: forget the committed rows
+            with torch.cuda.stream(stream if stream is not None else torch.cuda.current_stream()):
+                self.cached_len.copy_(self.prefix_len, non_blocking=True)
 
     def set_target(self, target_per_slot):
         t = np.zeros(self.cap, np.int32)
