@@ -66,6 +66,24 @@ def test_host_side_errors_need_no_gpu():
     assert elastic(I(0), F(-1.0), 1, 2, 4, wse) == pkg.ERR_INVALID_ARG
     assert elastic(I(2), F(float("nan")), 1, 2, 4, wse) == pkg.ERR_INVALID_ARG
     assert elastic(I(2), F(-1.0), 1, 2, 4, wse - 1) == pkg.ERR_WORKSPACE
+    # paged attention: page size not a power of two >= 32, missing block table
+    wsa = lib.echo_tree_verify_attn_workspace_size(1, 4, 8, 8, 128)
+    paged = lambda page, bt: lib.echo_tree_verify_attn_paged(
+        P(256), P(256), P(256), P(256), P(256), 8, page, bt, 4, P(256), P(256), P(256), 1, 1, 4,
+        8, 8, 128, 1.0, P(256), None, P(256), wsa, None, None)
+    assert paged(48, P(256)) == pkg.ERR_UNSUPPORTED
+    assert paged(16, P(256)) == pkg.ERR_UNSUPPORTED
+    assert paged(64, None) == pkg.ERR_INVALID_ARG
+    # acceptance from logits: vocab < 1, missing target output
+    al = lambda vocab, tgt: lib.echo_accept_logits(P(256), P(256), P(256), P(256), vocab, 1, 4, 4,
+                                                   tgt, P(256), P(256), P(256), None, None)
+    assert al(0, P(256)) == pkg.ERR_INVALID_ARG
+    assert al(100, None) == pkg.ERR_INVALID_ARG
+    # commit: misaligned K/V, max_depth out of range
+    cm = lambda kn, depth: lib.echo_commit_kv(P(256), P(256), P(256), depth, kn, P(256), 1, 4, 1,
+                                              P(256), P(256), 8, 16, P(256), 4, P(256), None, None)
+    assert cm(P(258), 4) == pkg.ERR_INVALID_ARG
+    assert cm(P(256), 17) == pkg.ERR_UNSUPPORTED
     assert lib.echo_tree_verify_attn_workspace_size(4, 20, 8, 8, 64) == 0
     assert lib.echo_tree_verify_attn(P(16), P(16), P(16), P(16), P(16), P(16), 10, P(16), P(16), 1,
                                      1, 4, 6, 4, 128, 1.0, P(16), None, P(256), 1 << 30, None,
