@@ -68,6 +68,7 @@ struct Unit {
 
 struct Cut {
   int32_t unit, b0, b1, first_slot;  // workgroups b0..b1; partial slot of b0's segment
+  Unit u;                            // the unit itself (the merge needs no second lookup)
 };
 
 struct AttnWs {
@@ -226,6 +227,7 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
     const int32_t* __restrict__ q_offsets, KvSource kv, int R, int hkv, int G, int max_rows,
     int nb, long long ucap, AttnWs ws, int32_t* status) {
   __shared__ int s_scan[kThreads / kWave + 1];
+  __shared__ int2 s_scan2[kThreads / kWave + 1];
   __shared__ uint8_t s_ok[ECHO_MAX_REQUESTS + 1];
   const int tid = threadIdx.x;
   int bits = 0;
@@ -238,14 +240,24 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
   }
   __syncthreads();
   auto ok_of = [&](int r) { return r < R && s_ok[r] != 0; };
+  // one request per thread (R <= 256, the usual case): shapes and their scans
+  // are computed once and kept for pass B
+  const bool single = R <= kThreads;
+  RequestShape s1 = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+  int ub1 = 0, tb1 = 0;
 
   // pass A: total units and tiles
   long long T = 0, U = 0;
   for (int base = 0; base < R; base += kThreads) {
     const RequestShape s = request_shape(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
     int tot_u, tot_t;
-    block_exclusive_sum<kThreads>(s.groups, s_scan, &tot_u);
-    block_exclusive_sum<kThreads>(s.groups * s.tiles, s_scan, &tot_t);
+    const int2 ex = block_exclusive_sum2<kThreads>(make_int2(s.groups, s.groups * s.tiles), s_scan2,
+                                                   &tot_u, &tot_t);
+    if (single) {
+      s1 = s;
+      ub1 = ex.x;
+      tb1 = ex.y;
+    }
     U += tot_u;
     T += tot_t;
   }
@@ -268,10 +280,21 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
   // pass B: units, the cut units and each workgroup's first unit
   int unit_run = 0, tile_run = 0, cut_run = 0;
   for (int base = 0; base < R; base += kThreads) {
-    const RequestShape s = request_shape(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
-    int tot_u, tot_t;
-    const int ub = unit_run + block_exclusive_sum<kThreads>(s.groups, s_scan, &tot_u);
-    const int tb = tile_run + block_exclusive_sum<kThreads>(s.groups * s.tiles, s_scan, &tot_t);
+    RequestShape s;
+    int ub, tb, tot_u, tot_t;
+    if (single) {
+      s = s1;
+      ub = ub1;
+      tb = tb1;
+      tot_u = int(U);
+      tot_t = int(T);
+    } else {
+      s = request_shape(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
+      const int2 ex = block_exclusive_sum2<kThreads>(make_int2(s.groups, s.groups * s.tiles),
+                                                     s_scan2, &tot_u, &tot_t);
+      ub = unit_run + ex.x;
+      tb = tile_run + ex.y;
+    }
     // a unit is cut if two workgroup ranges share it
     int ncut = 0;
     for (int g = 0; g < s.groups; ++g) {
@@ -303,6 +326,7 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
         cu.b0 = b0;
         cu.b1 = b1;
         cu.first_slot = range_lo(T, b0, nw) < u.tile_start ? 1 : 0;
+        cu.u = u;
         ws.cuts[c++] = cu;
       }
       // workgroups whose range starts inside this unit
@@ -875,7 +899,7 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv,
   const int rho = (e / (kD / 4)) % kPassRows;
   const int d4 = (e % (kD / 4)) * 4;
   const Cut c = ws.cuts[ci];
-  const Unit u = ws.units[c.unit];
+  const Unit& u = c.u;
   const Stream sm = stream_of(u, w, hkv, G);
   if (rho >= sm.rows) return;
   const int nparts = c.b1 - c.b0 + 1;

@@ -81,4 +81,44 @@ __device__ __forceinline__ int block_exclusive_sum(int v, int* scratch, int* tot
   return ex;
 }
 
+// Two exclusive prefix sums at once (same barriers as one); *total_x and
+// *total_y receive the block sums.  `scratch` holds NT/64 + 1 int2 of shared
+// memory.
+template <int NT>
+__device__ __forceinline__ int2 block_exclusive_sum2(int2 v, int2* scratch, int* total_x,
+                                                     int* total_y) {
+  constexpr int NW = NT / kWave;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wid = threadIdx.x / kWave;
+  int ix = v.x, iy = v.y;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int ux = __shfl_up(ix, off, kWave);
+    const int uy = __shfl_up(iy, off, kWave);
+    if (lane >= off) {
+      ix += ux;
+      iy += uy;
+    }
+  }
+  if (lane == kWave - 1) scratch[wid] = make_int2(ix, iy);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int rx = 0, ry = 0;
+    for (int w = 0; w < NW; ++w) {
+      const int2 t = scratch[w];
+      scratch[w] = make_int2(rx, ry);
+      rx += t.x;
+      ry += t.y;
+    }
+    scratch[NW] = make_int2(rx, ry);
+  }
+  __syncthreads();
+  const int2 base = scratch[wid];
+  const int2 tot = scratch[NW];
+  *total_x = tot.x;
+  *total_y = tot.y;
+  __syncthreads();
+  return make_int2(base.x + ix - v.x, base.y + iy - v.y);
+}
+
 }  // namespace echo
