@@ -1,17 +1,17 @@
 // Gate: path scores (eq. 5) and the global top-B selection under the batch
-// verification cap (eq. 4).  Four launches, none of which contends on a
+// verification cap (eq. 4).  Three launches, none of which contends on a
 // global atomic (on a multi-XCD part those serialise far from the CUs):
 //
 //   gate_score   one thread per candidate: root->leaf binary32 fold of the path
 //                score, 32-bit orderable key, and each block's 2048-bin histogram
 //                of the key's top 11 bits, written to its own slice.
-//   gate_bin     one block: from the blocks' finite counts and highest occupied
-//                bins, sums the block histograms downwards from the top in
-//                chunks of 64 bins until it finds the bin b* that holds the
-//                m-th largest key, m = min(B, #finite), and how many keys of b*
-//                are selected (usually one chunk: the selection is a small top).
-//   gate_select  one thread per candidate: keys above b* are selected, keys below
-//                are not; keys inside b* go to the block's own candidate slice.
+//   gate_select  one thread per candidate.  Every block first finds the bin b*
+//                that holds the m-th largest key, m = min(B, #finite): from the
+//                score blocks' finite counts and highest occupied bins it sums
+//                their histograms downwards from the top in chunks of 64 bins
+//                (usually one chunk: the selection is a small top).  Keys above
+//                b* are selected, keys below are not; keys inside b* go to the
+//                block's own candidate slice.
 //   gate_finish  one block: gathers the candidates into LDS, finds the
 //                threshold (key descending, index ascending) among them by radix
 //                selection, selects the head and checks the ancestor closure of
@@ -19,7 +19,7 @@
 //                selection runs over all keys in place.
 //
 // Sparse checkpoint gating (eq. 6, eq. 7; Alg. 1 phase 1) adds two launches in
-// front of gate_bin: gate_lmax_clear zeroes the per-(request, depth) maximum
+// front of gate_select: gate_lmax_clear zeroes the per-(request, depth) maximum
 // keys, gate_score then also folds each block's checkpoint-depth keys into
 // them (LDS first, one global atomicMax per block, request and depth) instead
 // of building histograms, and gate_trunc finds each request's first failed
@@ -328,11 +328,21 @@ __global__ __launch_bounds__(kGateThreads) void gate_trunc_kernel(const int32_t*
 constexpr int kChunkBins = 64;                         // bins per downward step
 constexpr int kChunkGroups = kGateThreads / kChunkBins;  // blocks summed in parallel per bin
 
-__global__ __launch_bounds__(kGateThreads) void gate_bin_kernel(int nblocks, int budget, GateWs ws,
-                                                               int32_t* __restrict__ num_selected) {
+// The threshold bin, computed by every select block (the histograms are small
+// and L2-resident; this saves a launch).  Block 0 records it for gate_finish.
+struct BinResult {
+  uint32_t m;     // min(B, #finite keys)
+  uint32_t bin;   // bin holding the m-th largest key
+  uint32_t need;  // keys of that bin that are selected
+  uint32_t cnt;   // keys in that bin
+};
+
+__device__ BinResult find_bin(int nblocks, int budget, const GateWs& ws, bool record,
+                              int32_t* num_selected) {
   __shared__ uint32_t s_part[kChunkGroups][kChunkBins];
   __shared__ uint2 s_red[kGateThreads / kWave];
-  __shared__ uint32_t s_state[3];  // running count above the chunk, found flag
+  __shared__ uint32_t s_state[2];  // keys in the bins above the current chunk, found flag
+  __shared__ BinResult s_res;
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1);
   // 1. #finite keys and the highest occupied bin over all score blocks
@@ -358,80 +368,92 @@ __global__ __launch_bounds__(kGateThreads) void gate_bin_kernel(int nblocks, int
   }
   const uint32_t m = min(uint32_t(budget), fin);
   if (t == 0) {
-    ws.meta->num_selected = int32_t(m);
-    ws.meta->bin = 0u;
-    ws.meta->bin_need = 0u;
-    ws.meta->bin_cnt = 0u;
-    ws.meta->thr_key = 0xFFFFFFFFu;
-    ws.meta->thr_g = -1;
-    *num_selected = int32_t(m);
-    s_state[0] = 0u;  // keys in the bins above the current chunk
-    s_state[1] = 0u;  // found
+    s_res.m = m;
+    s_res.bin = 0u;
+    s_res.need = 0u;
+    s_res.cnt = 0u;
+    s_state[0] = 0u;
+    s_state[1] = 0u;
   }
   __syncthreads();
-  if (m == 0u) return;
-  // 2. from the highest occupied bin downwards, 64 bins at a time
-  const int j = t % kChunkBins;   // bin offset below the chunk's top
-  const int grp = t / kChunkBins;  // blocks grp, grp + 16, ...
-  for (int hi = int(top) - 1; hi >= 0; hi -= kChunkBins) {
-    const int bin = hi - j;
-    uint32_t c = 0u;
-    if (bin >= 0) {
+  if (m != 0u) {
+    // 2. from the highest occupied bin downwards, 64 bins at a time
+    const int j = t % kChunkBins;    // bin offset below the chunk's top
+    const int grp = t / kChunkBins;  // blocks grp, grp + 16, ...
+    for (int hi = int(top) - 1; hi >= 0; hi -= kChunkBins) {
+      const int bin = hi - j;
+      uint32_t c = 0u;
+      if (bin >= 0) {
 #pragma unroll 4
-      for (int b = grp; b < nblocks; b += kChunkGroups) c += ws.bhist[size_t(b) * kHistBins + bin];
-    }
-    s_part[grp][j] = c;
-    __syncthreads();
-    if (t < kWave) {  // one wave scans the chunk's 64 bins, highest first
-      uint32_t cnt = 0u;
-#pragma unroll
-      for (int g = 0; g < kChunkGroups; ++g) cnt += s_part[g][t];
-      uint32_t incl = cnt;  // inclusive sum over bins hi .. hi - t
-#pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) {
-        const uint32_t u = __shfl_up(incl, off, kWave);
-        if (t >= off) incl += u;
+        for (int b = grp; b < nblocks; b += kChunkGroups) c += ws.bhist[size_t(b) * kHistBins + bin];
       }
-      const uint32_t above = s_state[0];
-      const bool cross = above + incl >= m && above + incl - cnt < m;
-      if (cross) {
-        ws.meta->bin = uint32_t(hi - t);
-        ws.meta->bin_cnt = cnt;
-        ws.meta->bin_need = m - (above + incl - cnt);
-        s_state[1] = 1u;
+      s_part[grp][j] = c;
+      __syncthreads();
+      if (t < kWave) {  // one wave scans the chunk's 64 bins, highest first
+        uint32_t cnt = 0u;
+#pragma unroll
+        for (int g = 0; g < kChunkGroups; ++g) cnt += s_part[g][t];
+        uint32_t incl = cnt;  // inclusive sum over bins hi .. hi - t
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+          const uint32_t u = __shfl_up(incl, off, kWave);
+          if (t >= off) incl += u;
+        }
+        const uint32_t above = s_state[0];
+        const bool cross = above + incl >= m && above + incl - cnt < m;
+        if (cross) {
+          s_res.bin = uint32_t(hi - t);
+          s_res.cnt = cnt;
+          s_res.need = m - (above + incl - cnt);
+          s_state[1] = 1u;
+        }
+        const uint32_t total = __shfl(incl, kWave - 1, kWave);
+        if (t == 0) s_state[0] = above + total;
       }
-      const uint32_t total = __shfl(incl, kWave - 1, kWave);
-      if (t == 0) s_state[0] = above + total;
+      __syncthreads();
+      if (s_state[1] != 0u) break;
+      __syncthreads();  // s_part is rewritten by the next chunk
     }
-    __syncthreads();
-    if (s_state[1] != 0u) break;
-    __syncthreads();  // s_part is rewritten by the next chunk
   }
+  const BinResult r = s_res;
+  if (record && t == 0) {
+    ws.meta->num_selected = int32_t(r.m);
+    ws.meta->bin = r.bin;
+    ws.meta->bin_need = r.need;
+    ws.meta->bin_cnt = r.cnt;
+    ws.meta->thr_key = 0xFFFFFFFFu;
+    ws.meta->thr_g = -1;
+    *num_selected = int32_t(r.m);
+  }
+  return r;
 }
 
 // --------------------------------------------------------------- select ----
-__global__ __launch_bounds__(kGateThreads) void gate_select_kernel(int N, GateWs ws,
+__global__ __launch_bounds__(kGateThreads) void gate_select_kernel(int N, int nblocks, int budget,
+                                                                   GateWs ws,
                                                                    uint8_t* __restrict__ selected,
+                                                                   int32_t* __restrict__ num_selected,
                                                                    int32_t* status) {
   __shared__ uint32_t s_cnt;
-  const uint32_t m = uint32_t(ws.meta->num_selected);
-  const uint32_t bin = ws.meta->bin;
   const int g = blockIdx.x * kGateThreads + threadIdx.x;
-  int bits = 0;
+  // this thread's key and parent are fetched while the bin is found
+  const uint32_t k = g < N ? ws.keys[g] : 0u;
+  const int32_t p = g < N ? ws.pglob[g] : -1;
   if (threadIdx.x == 0) s_cnt = 0u;
-  __syncthreads();
+  const BinResult br = find_bin(nblocks, budget, ws, blockIdx.x == 0, num_selected);
+  const uint32_t m = br.m;
+  const uint32_t bin = br.bin;
+  int bits = 0;
   if (g < N) {
-    const uint32_t k = ws.keys[g];
     const uint32_t kb = k >> kHistShift;
     if (m == 0u || k == 0u || kb < bin) {
       selected[g] = 0;
     } else if (kb > bin) {
       selected[g] = 1;
-      const int32_t p = ws.pglob[g];
       // a parent's key is never below its child's, so it lies in a higher bin too
       if (p >= 0 && !(ws.keys[p] >> kHistShift > bin)) bits |= ECHO_DATA_NOT_CLOSED;
     } else {
-      const uint32_t slot = atomicAdd(&s_cnt, 1u);  // LDS; the order is fixed by the sort
+      const uint32_t slot = atomicAdd(&s_cnt, 1u);  // LDS; the order is fixed by the finish
       ws.cand[size_t(blockIdx.x) * kGateThreads + slot] = make_uint2(k, uint32_t(g));
     }
   }
@@ -658,11 +680,9 @@ int32_t launch_gate(const int32_t* cand_offsets, const int32_t* parent, const fl
   if (sp.enabled)
     hipLaunchKernelGGL(gate_trunc_kernel, dim3(blocks), dim3(kGateThreads), lds, stream,
                        cand_offsets, R, N, ws, sp);
-  hipLaunchKernelGGL(gate_bin_kernel, dim3(1), dim3(kGateThreads), 0, stream, blocks, budget, ws,
-                     num_selected);
+  hipLaunchKernelGGL(gate_select_kernel, dim3(blocks), dim3(kGateThreads), 0, stream, N, blocks,
+                     budget, ws, selected, num_selected, status);
   if (N > 0) {
-    hipLaunchKernelGGL(gate_select_kernel, dim3(blocks), dim3(kGateThreads), 0, stream, N, ws,
-                       selected, status);
     hipLaunchKernelGGL(gate_finish_kernel, dim3(1), dim3(kGateThreads), 0, stream, N, blocks, ws,
                        selected, status);
   }
