@@ -54,7 +54,9 @@ def log(msg):
 
 
 def attn_algorithmic(batch, res, cfg):
-    """Algorithmic HBM bytes and FLOPs of one attention call."""
+    """Algorithmic HBM bytes and FLOPs of one attention call: the prefix K and V
+    once (bf16), plus per verify slot its q, new k/v, fp32 output and LSE; FLOPs
+    are 4 * D * Hq per visible key of every slot (QK^T and PV)."""
     import numpy as np
     qo = res["q_offsets"]
     P = batch["prefix_len"].astype(np.int64)
@@ -165,8 +167,8 @@ def main():
                          "reference kernel that scales the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no "
-              "multi-GPU path: the verification step runs on a single MI355X.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the verification "
+              "step runs on a single MI355X and there is no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
