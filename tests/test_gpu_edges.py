@@ -155,6 +155,29 @@ def test_crowded_threshold_bin():
         _check_all(b, attention=False)
 
 
+@pytest.mark.parametrize("budget", [5000, 16384])
+def test_maximum_batch_and_budget(budget):
+    """R = 4095 requests (the limit; the attention plan takes its multi-pass
+    path beyond 256) with up to 9 candidates each, budgets up to 16384 (the
+    limit: 513 mask words per slot)."""
+    rng = np.random.default_rng(17)
+    pool = synth.micro_pool(rng, 4095, 9, p_neg_inf=0.05)
+    N = int(pool["cand_offsets"][-1])
+    print(f"[edges] max sizes R=4095 N={N} B={budget}", flush=True)
+    b = make_micro_batch(pool, budget, hq=8, hkv=2, p_range=(0, 40), seed=5)
+    ref = _front_ref(b)
+    st, res = gc.run_gpu(b, ref["target"])
+    gc.compare_front(res, ref, N)
+    assert res["status"] == ref["status"]
+    cfg = b["cfg"]
+    m = ref["mask"]
+    rows = gc.sample_rows(m["q_offsets"], rng, n_requests=6, n_extra=200)
+    ro, rl, _ = oracle.tree_verify_attn(b["q"], b["k_new"], b["v_new"], b["k_cache"],
+                                        b["v_cache"], b["kv_offsets"], m["q_offsets"],
+                                        m["tree_mask"], cfg.hq, cfg.hkv, b["sm_scale"], rows=rows)
+    gc.compare_attn(res["out"], res["lse"], ro, rl, rows)
+
+
 def test_empty_requests_and_prefixes():
     offs = np.array([0, 0, 4, 4, 7], np.int32)            # requests 0 and 2 have no candidates
     parent = np.array([-1, 0, 0, 1, -1, -1, 1], np.int32)

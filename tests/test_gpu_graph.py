@@ -30,7 +30,7 @@ def _same(a, b, nq):
 
 
 @pytest.mark.parametrize("name,mode", [("tiny", "plain"), ("l8b", "plain"), ("l8b", "sparse"),
-                                       ("tiny", "serve"), ("l70b", "serve")])
+                                       ("l8b", "elastic"), ("tiny", "serve"), ("l70b", "serve")])
 def test_graph_replays_match_eager(name, mode):
     import torch
     from paper_2604_09603_amd.step import VerifyStep
@@ -38,8 +38,10 @@ def test_graph_replays_match_eager(name, mode):
     b = synth.make_batch(name, 1)
     ref = gc.oracle_front(b)
     kw = {}
-    if mode == "sparse":
+    if mode in ("sparse", "elastic"):
         kw["checkpoints"] = [(1, -3.0), (3, -8.0)]
+    if mode == "elastic":
+        kw["elastic"] = (2, 8)
     if mode == "serve":
         kw.update(page_size=64, serve=True)
     st = VerifyStep(b, **kw)
