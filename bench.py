@@ -74,6 +74,16 @@ def attn_algorithmic(batch, res, cfg):
     return kv_bytes + row_bytes, flops
 
 
+def attn_source_hash():
+    """sha256 of what the attention kernel is built from: its source and the build
+    script (which holds its compiler flags)."""
+    h = hashlib.sha256()
+    for rel in (("paper_2604_09603_amd", "csrc", "attn.hip"), ("paper_2604_09603_amd", "build.py")):
+        with open(os.path.join(ROOT, *rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
 def traffic_from_profile(attn_src_hash):
     """HBM bytes per attention-kernel launch from the committed rocprofv3 PMC summary."""
     path = os.path.join(ROOT, "profiles", "attn_main_q235b_pmc.json")
@@ -283,9 +293,7 @@ def main():
     value = nq / (ms_step / 1000.0)
     bytes_alg, flops_alg = attn_algorithmic(batch, res, cfg)
     achieved_gbs = bytes_alg / (attn_us * 1e-6) / 1e9
-    with open(os.path.join(ROOT, "paper_2604_09603_amd", "csrc", "attn.hip"), "rb") as f:
-        attn_hash = hashlib.sha256(f.read()).hexdigest()
-    traffic = traffic_from_profile(attn_hash)
+    traffic = traffic_from_profile(attn_source_hash())
 
     out = {
         "metric": METRIC,

@@ -21,6 +21,15 @@ FLAGS = [
 ]
 
 
+# Per-file flags.  The attention kernel keeps its MFMA accumulators in VGPRs:
+# left to its heuristics the compiler holds them in AGPRs and copies all of them
+# to VGPRs and back on every tile (a v_accvgpr read and write per register),
+# which costs as many VALU cycles as the tile's MFMAs.
+FILE_FLAGS = {
+    "attn.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1"],
+}
+
+
 def _hipcc():
     path = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
     if not os.path.exists(path):
@@ -35,7 +44,7 @@ def build(verbose: bool = False) -> str:
 
     def compile_one(name):
         obj = os.path.join(BUILD, name[:-4] + ".o")
-        cmd = [hipcc, *FLAGS, "-c", os.path.join(CSRC, name), "-o", obj]
+        cmd = [hipcc, *FLAGS, *FILE_FLAGS.get(name, []), "-c", os.path.join(CSRC, name), "-o", obj]
         res = subprocess.run(cmd, capture_output=True, text=True)
         if res.returncode != 0:
             raise RuntimeError(f"hipcc failed for {name}:\n{res.stderr}")
