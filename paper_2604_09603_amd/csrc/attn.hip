@@ -25,7 +25,7 @@
 //                 v_mfma_f32_16x16x32_bf16 (fp32 accumulation), online softmax
 //                 in base 2, ancestor bitmask on tree-tail tiles.  A unit that
 //                 lies inside one range is normalised and written to out/lse; a
-//                 cut unit leaves one partial (O, max, sum) per stream and
+//                 cut unit leaves one partial (O, max, sums) per stream and
 //                 workgroup.
 //   attn_combine  one thread per (cut unit, stream, row, 4 dims): merges the
 //                 partials in range order (deterministic) into out and lse.
@@ -76,7 +76,7 @@ struct AttnWs {
   Unit* units;
   int32_t* wg_unit;  // [nb] unit holding each workgroup's first tile
   Cut* cuts;
-  float* part_ml;  // [2 * nb * 4 * 48][2]: softmax reference max (log2 units), sum
+  float* part_ml;  // [2 * nb * 4 * 48][4]: reference max (log2 units), sum, rounded sum, 0
   float* part_o;   // [2 * nb * 4 * 48][128]
 };
 
@@ -104,14 +104,14 @@ __host__ __device__ inline AttnWs attn_layout(void* base, size_t ucap, int nb) {
   w.cuts = reinterpret_cast<Cut*>(p);
   p += al(size_t(nb) * sizeof(Cut));
   w.part_ml = reinterpret_cast<float*>(p);
-  p += al(part_rows(nb) * 2 * sizeof(float));
+  p += al(part_rows(nb) * 4 * sizeof(float));
   w.part_o = reinterpret_cast<float*>(p);
   return w;
 }
 
 __host__ inline size_t attn_ws_total(size_t ucap, int nb) {
   return 256 + al(ucap * sizeof(Unit)) + al(size_t(nb) * 4) + al(size_t(nb) * sizeof(Cut)) +
-         al(part_rows(nb) * 2 * 4) + al(part_rows(nb) * kD * 4);
+         al(part_rows(nb) * 4 * 4) + al(part_rows(nb) * kD * 4);
 }
 
 // Partial row of (workgroup b, slot, stream w, row rho).
@@ -361,11 +361,17 @@ static_assert(kMainLds <= 160 * 1024, "gfx950 LDS per workgroup");
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Round two floats to bfloat16 (to nearest even) in one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  __bf16 a = static_cast<__bf16>(lo);
-  __bf16 b = static_cast<__bf16>(hi);
-  return uint32_t(__builtin_bit_cast(uint16_t, a)) |
-         (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{lo, hi}, bf16x2));
+}
+
+// Sum of the two bfloat16 values packed in a word, in float.
+__device__ __forceinline__ float sum_bf16x2(uint32_t w) {
+  return __uint_as_float(w << 16) + __uint_as_float(w & 0xFFFF0000u);
 }
 
 __device__ __forceinline__ int swz(int row, int chunk) {
@@ -457,7 +463,8 @@ __device__ __forceinline__ void wait_lds() {
 struct RowTile {
   floatx4 o[8];  // O^T: lane holds dims 16*dt + 4*(lane/16) + i of row lane%16
   float m;       // softmax reference max of scaled logits (log2 units)
-  float l;       // this lane's share of the running sum
+  float l;       // this lane's share of the running sum (for the LSE)
+  float lq;      // the same over the bf16-rounded probabilities (normalises O)
 };
 
 // Per-lane LDS byte offsets of the swizzled fragment reads (lane constants; the
@@ -579,6 +586,7 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
     if (__ballot(grow) != 0ull) {
       const float alpha = grow ? __builtin_amdgcn_exp2f(rt[t].m - mt) : 1.0f;  // 0 from -inf
       rt[t].l *= alpha;
+      rt[t].lq *= alpha;
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) rt[t].o[dt] *= alpha;
       rt[t].m = grow ? mt : rt[t].m;
@@ -596,6 +604,14 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
     pk.y = pack_bf16x2(sv[2], sv[3]);
     pk.z = pack_bf16x2(sv[4], sv[5]);
     pk.w = pack_bf16x2(sv[6], sv[7]);
+    // O is normalised by the sum of the same rounded probabilities that
+    // multiply V, so the output is an exact convex combination of V rows with
+    // the rounded weights: each weight is off by at most 2^-8 of itself and the
+    // output by at most 2^-9 times the spread of the V values that carry the
+    // weight.  (Dividing by the unrounded sum leaves an error of up to 2^-9 of
+    // |v| even on a row whose weight sits on one key.)  The LSE keeps the
+    // unrounded sum.
+    rt[t].lq += (sum_bf16x2(pk.x) + sum_bf16x2(pk.y)) + (sum_bf16x2(pk.z) + sum_bf16x2(pk.w));
     pf[t] = as_bf16x8(pk);
   }
   // O^T += V^T P^T
@@ -754,6 +770,7 @@ __device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws,
     for (int dt = 0; dt < 8; ++dt) rt[i].o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
     rt[i].m = -__builtin_inff();
     rt[i].l = 0.0f;
+    rt[i].lq = 0.0f;
   }
   wait_vm<0>();
 
@@ -803,13 +820,14 @@ __device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws,
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
     const float L = row_sum4(rt[i].l);
+    const float Lq = row_sum4(rt[i].lq);
     const float M = rt[i].m;
     const int rho = 16 * i + lr;
     if (rho < sm.rows) {
       if (!cut) {
         const int ra = sm.row0 + rho;
         const size_t orow = size_t(ud.q0 + ra / G) * a.hq + sm.kvh * G + ra % G;
-        const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+        const float inv = Lq > 0.0f ? 1.0f / Lq : 0.0f;
         float* po = a.out + orow * kD;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt)
@@ -822,10 +840,8 @@ __device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws,
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt)
           *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = rt[i].o[dt];
-        if (lg == 0) {
-          ws.part_ml[prow * 2 + 0] = M;
-          ws.part_ml[prow * 2 + 1] = L;
-        }
+        if (lg == 0)
+          *reinterpret_cast<floatx4*>(ws.part_ml + prow * 4) = floatx4{M, L, Lq, 0.0f};
       }
     }
   }
@@ -909,52 +925,54 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv,
   const size_t orow = size_t(u.q0 + ra / G) * hq + sm.kvh * G + ra % G;
   if (nparts <= kFastParts) {
     // every load issued at once: one memory round trip
-    float2 ml[kFastParts];
+    floatx4 ml[kFastParts];  // reference max, sum, rounded sum
     floatx4 po[kFastParts];
 #pragma unroll
     for (int i = 0; i < kFastParts; ++i) {
-      ml[i] = make_float2(-__builtin_inff(), 0.0f);
+      ml[i] = floatx4{-__builtin_inff(), 0.0f, 0.0f, 0.0f};
       po[i] = floatx4{0.f, 0.f, 0.f, 0.f};
       if (i < nparts) {
         const size_t prow = prow_of(i);
-        ml[i] = *reinterpret_cast<const float2*>(ws.part_ml + prow * 2);
+        ml[i] = *reinterpret_cast<const floatx4*>(ws.part_ml + prow * 4);
         po[i] = *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
       }
     }
     float M = -__builtin_inff();
 #pragma unroll
-    for (int i = 0; i < kFastParts; ++i) M = fmaxf(M, ml[i].x);
-    float L = 0.0f;
+    for (int i = 0; i < kFastParts; ++i) M = fmaxf(M, ml[i][0]);
+    float L = 0.0f, Lq = 0.0f;
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
     if (M != -__builtin_inff()) {
 #pragma unroll
       for (int i = 0; i < kFastParts; ++i) {
-        if (ml[i].x == -__builtin_inff()) continue;  // absent or empty part
-        const float wgt = __builtin_amdgcn_exp2f(ml[i].x - M);
-        L += wgt * ml[i].y;
+        if (ml[i][0] == -__builtin_inff()) continue;  // absent or empty part
+        const float wgt = __builtin_amdgcn_exp2f(ml[i][0] - M);
+        L += wgt * ml[i][1];
+        Lq += wgt * ml[i][2];
         acc += wgt * po[i];
       }
     }
-    const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+    const float inv = Lq > 0.0f ? 1.0f / Lq : 0.0f;
     *reinterpret_cast<floatx4*>(out + orow * kD + d4) = acc * inv;
     if (lse != nullptr && d4 == 0) lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
     return;
   }
   float M = -__builtin_inff();
-  for (int i = 0; i < nparts; ++i) M = fmaxf(M, ws.part_ml[prow_of(i) * 2]);
-  float L = 0.0f;
+  for (int i = 0; i < nparts; ++i) M = fmaxf(M, ws.part_ml[prow_of(i) * 4]);
+  float L = 0.0f, Lq = 0.0f;
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
   if (M != -__builtin_inff()) {
     for (int i = 0; i < nparts; ++i) {
       const size_t prow = prow_of(i);
-      const float2 ml = *reinterpret_cast<const float2*>(ws.part_ml + prow * 2);
-      if (ml.x == -__builtin_inff()) continue;
-      const float wgt = __builtin_amdgcn_exp2f(ml.x - M);
-      L += wgt * ml.y;
+      const floatx4 ml = *reinterpret_cast<const floatx4*>(ws.part_ml + prow * 4);
+      if (ml[0] == -__builtin_inff()) continue;
+      const float wgt = __builtin_amdgcn_exp2f(ml[0] - M);
+      L += wgt * ml[1];
+      Lq += wgt * ml[2];
       acc += wgt * *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
     }
   }
-  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+  const float inv = Lq > 0.0f ? 1.0f / Lq : 0.0f;
   *reinterpret_cast<floatx4*>(out + orow * kD + d4) = acc * inv;
   if (lse != nullptr && d4 == 0) lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
 }
