@@ -369,38 +369,21 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{lo, hi}, bf16x2));
 }
 
-// Sum of the two bfloat16 values packed in a word, in float.
-__device__ __forceinline__ float sum_bf16x2(uint32_t w) {
-  return __uint_as_float(w << 16) + __uint_as_float(w & 0xFFFF0000u);
+// acc plus the two bfloat16 values packed in w (one v_dot2c_f32_bf16 against
+// (1, 1); the products are exact).
+__device__ __forceinline__ float add_bf16x2(uint32_t w, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w),
+                                         __builtin_bit_cast(bf16x2, 0x3F803F80u), acc, false);
 }
 
 __device__ __forceinline__ int swz(int row, int chunk) {
   return row * 256 + ((chunk ^ (row & 15)) << 4);
 }
 
-// One direct HBM -> LDS copy instruction: every lane moves 16 bytes from
-// base + voff (base uniform in the wave, voff per lane) to lds_dst + 16 * lane.
-// Issued through inline assembly so that the compiler does not track it: its
-// own bookkeeping would otherwise drain every copy in flight before each LDS
-// read.  Completion is awaited explicitly (vmcnt).
 __device__ __forceinline__ uint64_t uniform64(uint64_t x) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(x));
   const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(x >> 32));
   return (uint64_t(hi) << 32) | lo;
-}
-
-__device__ __forceinline__ void dma16(uint64_t base, uint32_t voff, const char* lds_dst) {
-  // the LDS destination is uniform in the wave; make that explicit for the SGPR operand
-  const uint32_t lds = __builtin_amdgcn_readfirstlane(
-      uint32_t(reinterpret_cast<uintptr_t>((const lds_void_t*)lds_dst)));
-  const uint64_t sbase = uniform64(base);
-  uint32_t saved;  // M0 belongs to the compiler: restore it
-  asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %2, %3\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "s"(lds), "v"(voff), "s"(sbase)
-      : "memory");
 }
 
 constexpr int kCopiesPerTile = 16;  // wave instructions of 1 KB (4 key rows) per K+V tile
@@ -427,24 +410,53 @@ __device__ __forceinline__ CopyPlan copy_plan(uint32_t row_bytes) {
   return cp;
 }
 
-// Copy one K+V tile (tn <= 32 valid key rows, rows row_bytes apart) into a
-// stage.  Rows >= tn re-read row tn-1 (in bounds); the softmax masks those keys.
-__device__ __forceinline__ void issue_tile(char* stage, uint64_t kbase, uint64_t vbase,
+// One K+V tile into a stage with 16 direct HBM -> LDS loads: in load j every
+// lane moves 16 bytes from kbase + off[j] (V: vbase + off[j]) to 1 KB block j
+// (V: block 8 + j) of the stage, at lds_stage + 1024 * block + 16 * lane.  The
+// bases and lds_stage are wave-uniform, the offsets per lane.  One inline
+// assembly block issues them, for two reasons: the compiler does not track
+// these loads (its own bookkeeping would drain every load in flight before each
+// LDS read; completion is awaited explicitly with vmcnt), and M0, which holds
+// the LDS address of such a load, is set once and stepped by 1 KB.  A write of
+// M0 needs one wait state before an LDS load reads it (s_nop 0).  M0 belongs to
+// the compiler and is restored; the steps clobber SCC.
+__device__ __forceinline__ void dma_tile(uint32_t lds_stage, uint64_t kbase, uint64_t vbase,
+                                         const uint32_t (&off)[8]) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_stage);
+  const uint64_t kb = uniform64(kbase), vb = uniform64(vbase);
+  uint32_t saved;
+#define ECHO_DMA_STEP(J, B) \
+  "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %" #J ", %" #B "\n\t"
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, %10\n\t"
+      ECHO_DMA_STEP(3, 10) ECHO_DMA_STEP(4, 10) ECHO_DMA_STEP(5, 10) ECHO_DMA_STEP(6, 10)
+      ECHO_DMA_STEP(7, 10) ECHO_DMA_STEP(8, 10) ECHO_DMA_STEP(9, 10)
+      ECHO_DMA_STEP(2, 11) ECHO_DMA_STEP(3, 11) ECHO_DMA_STEP(4, 11) ECHO_DMA_STEP(5, 11)
+      ECHO_DMA_STEP(6, 11) ECHO_DMA_STEP(7, 11) ECHO_DMA_STEP(8, 11) ECHO_DMA_STEP(9, 11)
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "v"(off[4]),
+        "v"(off[5]), "v"(off[6]), "v"(off[7]), "s"(kb), "s"(vb)
+      : "memory", "scc");
+#undef ECHO_DMA_STEP
+}
+
+// Copy one K+V tile (tn <= 32 valid key rows, rows row_bytes apart) into the
+// stage at LDS address lds_stage.  Rows >= tn re-read row tn-1 (in bounds); the
+// softmax masks those keys.
+__device__ __forceinline__ void issue_tile(uint32_t lds_stage, uint64_t kbase, uint64_t vbase,
                                            uint32_t row_bytes, int tn, const CopyPlan& cp) {
   if (tn == kTileKeys) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) dma16(kbase, cp.off[j], stage + j * 1024);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) dma16(vbase, cp.off[j], stage + kTileBytes + j * 1024);
+    dma_tile(lds_stage, kbase, vbase, cp.off);
   } else {
+    uint32_t off[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int row = copy_row(j);
       const int srow = row < tn ? row : tn - 1;
-      const uint32_t off = uint32_t(srow) * row_bytes + copy_chunk16(row);
-      dma16(kbase, off, stage + j * 1024);
-      dma16(vbase, off, stage + kTileBytes + j * 1024);
+      off[j] = uint32_t(srow) * row_bytes + copy_chunk16(row);
     }
+    dma_tile(lds_stage, kbase, vbase, off);
   }
 }
 
@@ -611,7 +623,7 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
     // weight.  (Dividing by the unrounded sum leaves an error of up to 2^-9 of
     // |v| even on a row whose weight sits on one key.)  The LSE keeps the
     // unrounded sum.
-    rt[t].lq += (sum_bf16x2(pk.x) + sum_bf16x2(pk.y)) + (sum_bf16x2(pk.z) + sum_bf16x2(pk.w));
+    rt[t].lq = add_bf16x2(pk.w, add_bf16x2(pk.z, add_bf16x2(pk.y, add_bf16x2(pk.x, rt[t].lq))));
     pf[t] = as_bf16x8(pk);
   }
   // O^T += V^T P^T
@@ -672,50 +684,68 @@ __device__ __forceinline__ Unit load_unit(const Unit* units, int i) {
 struct Issuer {
   int iu;          // unit of the next tile to copy (wave-uniform)
   Unit ud;
+  Stream sm;       // this wave's stream of that unit
   int k;           // ordinal of the next tile to copy
   uint32_t copied;  // bit s: the last copy into stage s moved data
+  // the stream's KV head: at the unit's first new-key row, and at its first
+  // prefix row (contiguous cache) or at row 0 of the cache (paged)
+  const char *tail_k, *tail_v, *pre_k, *pre_v;
+  const int32_t* bt_row;  // paged: the request's block-table row
 };
 
+// Point the issue side at unit is.ud.
+__device__ __forceinline__ void issuer_unit(Issuer& is, const MainArgs& a, int wid) {
+  is.sm = stream_of(is.ud, wid, a.hkv, a.G);
+  const size_t row_bytes = size_t(a.hkv) * kD * 2;
+  const size_t head = size_t(is.sm.kvh) * kD * 2;
+  is.tail_k = reinterpret_cast<const char*>(a.k_new) + size_t(is.ud.q0) * row_bytes + head;
+  is.tail_v = reinterpret_cast<const char*>(a.v_new) + size_t(is.ud.q0) * row_bytes + head;
+  const size_t first = a.block_table == nullptr ? size_t(is.ud.kb) * row_bytes : 0;
+  is.pre_k = reinterpret_cast<const char*>(a.k_cache) + first + head;
+  is.pre_v = reinterpret_cast<const char*>(a.v_cache) + first + head;
+  is.bt_row = a.block_table == nullptr ? nullptr
+                                       : a.block_table + size_t(is.ud.kb) * size_t(a.max_pages);
+}
+
 __device__ __forceinline__ void issue_next(Issuer& is, const MainArgs& a, const AttnWs& ws,
-                                           int nunits, int lo, int hi, int wid, char* ring,
-                                           const CopyPlan& cp) {
+                                           int nunits, int lo, int hi, int wid,
+                                           uint32_t ring_lds, const CopyPlan& cp) {
   const int t = lo + is.k;
   if (t >= hi) return;
   while (t >= is.ud.tile_end && is.iu + 1 < nunits) {
     is.iu = __builtin_amdgcn_readfirstlane(is.iu + 1);
     is.ud = load_unit(ws.units, is.iu);
+    issuer_unit(is, a, wid);
   }
   const int lt = t - is.ud.tile_start;
-  const Stream sm = stream_of(is.ud, wid, a.hkv, a.G);
-  const bool copy = sm.rows > 0 && lt >= 0 && t < is.ud.tile_end;
+  const bool copy = is.sm.rows > 0 && lt >= 0 && t < is.ud.tile_end;
   is.copied = (is.copied & ~(1u << (is.k & 1))) | (uint32_t(copy) << (is.k & 1));
   if (copy) {
-    const size_t stride = size_t(a.hkv) * kD;
-    const uint16_t *kb, *vb;
+    const uint32_t row_bytes = uint32_t(a.hkv) * kD * 2;
+    const uint32_t tile_bytes = kTileKeys * row_bytes;
+    const char *kb, *vb;
     int tn;
     if (lt < is.ud.ntail) {
-      const size_t row = size_t(is.ud.q0) + size_t(lt) * kTileKeys;
-      kb = a.k_new + row * stride + sm.kvh * kD;
-      vb = a.v_new + row * stride + sm.kvh * kD;
+      kb = is.tail_k + size_t(lt) * tile_bytes;
+      vb = is.tail_v + size_t(lt) * tile_bytes;
       tn = min(kTileKeys, is.ud.nslots - lt * kTileKeys);
     } else {
       const int pt = lt - is.ud.ntail;
-      size_t row;
-      if (a.block_table == nullptr) {
-        row = size_t(is.ud.kb) + size_t(pt) * kTileKeys;
+      size_t off;
+      if (is.bt_row == nullptr) {
+        off = size_t(pt) * tile_bytes;
       } else {
         // wave-uniform index: a scalar load of the tile's page
         const int pos = pt * kTileKeys;
-        const const_i32_t* bt = (const const_i32_t*)(a.block_table);
-        const int page = bt[size_t(is.ud.kb) * size_t(a.max_pages) + size_t(pos >> a.page_shift)];
-        row = (size_t(page) << a.page_shift) + size_t(pos & ((1 << a.page_shift) - 1));
+        const int page = ((const const_i32_t*)is.bt_row)[pos >> a.page_shift];
+        off = ((size_t(page) << a.page_shift) + size_t(pos & ((1 << a.page_shift) - 1))) * row_bytes;
       }
-      kb = a.k_cache + row * stride + sm.kvh * kD;
-      vb = a.v_cache + row * stride + sm.kvh * kD;
+      kb = is.pre_k + off;
+      vb = is.pre_v + off;
       tn = min(kTileKeys, is.ud.P - pt * kTileKeys);
     }
-    issue_tile(ring + (is.k & 1) * kStageBytes, reinterpret_cast<uint64_t>(kb),
-               reinterpret_cast<uint64_t>(vb), uint32_t(stride * 2), tn, cp);
+    issue_tile(ring_lds + uint32_t((is.k & 1) * kStageBytes), reinterpret_cast<uint64_t>(kb),
+               reinterpret_cast<uint64_t>(vb), row_bytes, tn, cp);
   }
   ++is.k;
 }
@@ -733,7 +763,8 @@ __device__ __forceinline__ uint32_t mask_word(const MainArgs& a, const Unit& ud,
 template <int MT>
 __device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws, const Unit& ud,
                                             const Stream& sm, int seg_lo, int seg_hi, int lo,
-                                            int hi, int nunits, int b, char* ring, Issuer& is,
+                                            int hi, int nunits, int b, const char* ring,
+                                            uint32_t ring_lds, Issuer& is,
                                             const CopyPlan& cp, const LaneOffsets& lof) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wid = wave_id();
@@ -810,7 +841,7 @@ __device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws,
     TileFrags f;
     load_tile(stg, stg + kTileBytes, lof, f);
     wait_lds();
-    issue_next(is, a, ws, nunits, lo, hi, wid, ring, cp);
+    issue_next(is, a, ws, nunits, lo, hi, wid, ring_lds, cp);
     compute_tile<MT>(f, qf, rt, masked, tn, a.scale2, word);
   }
 
@@ -862,6 +893,9 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
   const CopyPlan cp = copy_plan(uint32_t(a.hkv) * kD * 2);
   const LaneOffsets lof = lane_offsets();
   char* ring = smem + wid * (kWaveStages * kStageBytes);
+  // the ring's LDS address (wave-uniform), for the copies
+  const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(
+      uint32_t(reinterpret_cast<uintptr_t>((lds_void_t*)ring)));
   const int nunits = ws.meta[0];
 
   // the wave walks the units from the one holding the range's first tile; the
@@ -870,10 +904,11 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
   Issuer is;
   is.iu = first_unit;
   is.ud = load_unit(ws.units, is.iu);
+  issuer_unit(is, a, wid);
   is.k = 0;
   is.copied = 0u;
 #pragma unroll
-  for (int s = 0; s < kWaveStages; ++s) issue_next(is, a, ws, nunits, lo, hi, wid, ring, cp);
+  for (int s = 0; s < kWaveStages; ++s) issue_next(is, a, ws, nunits, lo, hi, wid, ring_lds, cp);
 
   int u = first_unit;
   while (true) {
@@ -884,13 +919,13 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
     const int mt = (sm.rows + 15) / 16;
     if (mt == 0) {
       // empty stream: nothing was copied for these tiles; keep the ring moving
-      for (int t = seg_lo; t < seg_hi; ++t) issue_next(is, a, ws, nunits, lo, hi, wid, ring, cp);
+      for (int t = seg_lo; t < seg_hi; ++t) issue_next(is, a, ws, nunits, lo, hi, wid, ring_lds, cp);
     } else if (mt == 1) {
-      run_segment<1>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, is, cp, lof);
+      run_segment<1>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof);
     } else if (mt == 2) {
-      run_segment<2>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, is, cp, lof);
+      run_segment<2>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof);
     } else {
-      run_segment<3>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, is, cp, lof);
+      run_segment<3>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof);
     }
     if (seg_hi >= hi || u + 1 >= nunits) break;
     u = __builtin_amdgcn_readfirstlane(u + 1);
