@@ -21,12 +21,17 @@ FLAGS = [
 ]
 
 
-# Per-file flags.  The attention kernel keeps its MFMA accumulators in VGPRs:
-# left to its heuristics the compiler holds them in AGPRs and copies all of them
-# to VGPRs and back on every tile (a v_accvgpr read and write per register),
-# which costs as many VALU cycles as the tile's MFMAs.
+# Per-file flags for the attention kernel:
+# * its MFMA accumulators stay in VGPRs: left to its heuristics the compiler
+#   holds them in AGPRs and copies all of them to VGPRs and back on every tile
+#   (a v_accvgpr read and write per register), which costs as many VALU cycles
+#   as the tile's MFMAs;
+# * no NaN semantics: with them every fmaxf over MFMA results (the softmax row
+#   maxima) is preceded by a v_max_f32 x, x, x that quiets signalling NaNs,
+#   about 50 extra VALU instructions per 64-row tile.  Infinities (masked keys
+#   are -inf) keep their meaning; NaN inputs give unspecified outputs.
 FILE_FLAGS = {
-    "attn.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1"],
+    "attn.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1", "-fno-honor-nans"],
 }
 
 

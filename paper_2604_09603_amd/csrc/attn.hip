@@ -3,7 +3,7 @@
 //
 //   attn_plan     one workgroup.  A stream is one KV head of one request
 //                 together with a pass over its rows (rows = verify slots x
-//                 query heads of the GQA group, at most 48 per pass).  The
+//                 query heads of the GQA group, at most 64 per pass).  The
 //                 streams of a request are grouped four at a time, head-major;
 //                 a group is one unit of work whose tiles are the request's
 //                 32-key tiles: first the tree-tail tiles (the new keys of the
@@ -27,7 +27,7 @@
 //                 lies inside one range is normalised and written to out/lse; a
 //                 cut unit leaves one partial (O, max, sums) per stream and
 //                 workgroup.
-//   attn_combine  one thread per (cut unit, stream, row, 4 dims): merges the
+//   attn_combine  one thread per (cut unit, stream, two rows, 4 dims): merges the
 //                 partials in range order (deterministic) into out and lse.
 #include <hip/hip_ext.h>
 
@@ -40,8 +40,8 @@ namespace {
 constexpr int kD = ECHO_HEAD_DIM;   // 128
 constexpr int kThreads = 256;       // plan / combine workgroups
 constexpr int kWaves = 4;           // main kernel: waves (streams) per workgroup, one per CU
-constexpr int kMaxMT = 3;           // 16-row tiles per stream (more would spill registers)
-constexpr int kPassRows = kMaxMT * 16;  // rows per stream (48)
+constexpr int kMaxMT = 4;           // 16-row tiles per stream (394 of the 512 registers a wave has)
+constexpr int kPassRows = kMaxMT * 16;  // rows per stream (64)
 constexpr int kWaveStages = 2;      // per-wave LDS ring depth (32-key K+V tiles)
 constexpr int kTileKeys = 32;       // keys per tile
 constexpr int kMaskWords = 2;       // tree-tail mask words preloaded per row and segment
@@ -76,8 +76,8 @@ struct AttnWs {
   Unit* units;
   int32_t* wg_unit;  // [nb] unit holding each workgroup's first tile
   Cut* cuts;
-  float* part_ml;  // [2 * nb * 4 * 48][4]: reference max (log2 units), sum, rounded sum, 0
-  float* part_o;   // [2 * nb * 4 * 48][128]
+  float* part_ml;  // [2 * nb * 4 * 64][4]: reference max (log2 units), sum, rounded sum, 0
+  float* part_o;   // [2 * nb * 4 * 64][128]
 };
 
 __host__ __device__ inline size_t al(size_t x) { return (x + 255) / 256 * 256; }
@@ -196,7 +196,7 @@ struct RequestShape {
   int groups, tiles, q0, nsl, kb, P, ntail, passes, rpp;
 };
 
-// A request's rows per head split into passes of at most 48 rows, as even as
+// A request's rows per head split into passes of at most 64 rows, as even as
 // possible; its hkv * passes streams form ceil(/4) groups over the same tiles.
 // `ok` is request_ok of request r (evaluated once per plan).  A paged request's
 // kb is its index (its block table row), a contiguous one's its first row.
@@ -924,8 +924,10 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
       run_segment<1>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof);
     } else if (mt == 2) {
       run_segment<2>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof);
-    } else {
+    } else if (mt == 3) {
       run_segment<3>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof);
+    } else {
+      run_segment<4>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof);
     }
     if (seg_hi >= hi || u + 1 >= nunits) break;
     u = __builtin_amdgcn_readfirstlane(u + 1);
@@ -933,12 +935,40 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
 }
 
 // ------------------------------------------------------------- combine ----
-// One thread per (cut unit, stream, row, 4 dims); a cut's items span
-// kCombineBlocks workgroups.  The partials are merged in workgroup order.
-constexpr int kCombineItems = kWaves * kPassRows * (kD / 4);
+// One thread per (cut unit, stream, pair of rows, 4 dims): rows rho and
+// rho + 32 of the stream; a cut's items span kCombineBlocks workgroups.  The
+// partials are merged in workgroup order.
+constexpr int kCombineRowsPerThread = 2;
+constexpr int kCombineItems = kWaves * (kPassRows / kCombineRowsPerThread) * (kD / 4);
 constexpr int kCombineBlocks = kCombineItems / kThreads;
 constexpr int kFastParts = 4;  // cuts over at most this many workgroups merge in one round trip
 static_assert(kCombineItems % kThreads == 0, "combine tiling");
+
+// One output row (4 dims) and its LSE from the partials of its parts: (max,
+// sum, rounded sum) and O of each (parts with max -inf are absent or empty).
+template <int NP>
+__device__ __forceinline__ void merge_parts(const floatx4 (&ml)[NP], const floatx4 (&po)[NP],
+                                            int np, float* o, float* l) {
+  float M = -__builtin_inff();
+#pragma unroll
+  for (int i = 0; i < NP; ++i)
+    if (i < np) M = fmaxf(M, ml[i][0]);
+  float L = 0.0f, Lq = 0.0f;
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (M != -__builtin_inff()) {
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      if (i >= np || ml[i][0] == -__builtin_inff()) continue;
+      const float wgt = __builtin_amdgcn_exp2f(ml[i][0] - M);
+      L += wgt * ml[i][1];
+      Lq += wgt * ml[i][2];
+      acc += wgt * po[i];
+    }
+  }
+  const float inv = Lq > 0.0f ? 1.0f / Lq : 0.0f;
+  *reinterpret_cast<floatx4*>(o) = acc * inv;
+  if (l != nullptr) *l = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
+}
 
 __global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv, int G, AttnWs ws,
                                                                 float* __restrict__ out,
@@ -946,70 +976,75 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv,
   const int ci = blockIdx.x / kCombineBlocks;
   if (ci >= ws.meta[2]) return;
   const int e = (blockIdx.x % kCombineBlocks) * kThreads + threadIdx.x;
-  const int w = e / (kPassRows * (kD / 4));
-  const int rho = (e / (kD / 4)) % kPassRows;
+  constexpr int kRowSpan = kPassRows / kCombineRowsPerThread;
+  constexpr int NR = kCombineRowsPerThread;
+  const int w = e / (kRowSpan * (kD / 4));
+  const int rho0 = (e / (kD / 4)) % kRowSpan;
   const int d4 = (e % (kD / 4)) * 4;
   const Cut c = ws.cuts[ci];
   const Unit& u = c.u;
   const Stream sm = stream_of(u, w, hkv, G);
-  if (rho >= sm.rows) return;
+  if (rho0 >= sm.rows) return;
   const int nparts = c.b1 - c.b0 + 1;
   // partial of part i: workgroup b0 + i, whose segment may sit in its second slot
-  auto prow_of = [&](int i) { return part_row(c.b0 + i, i == 0 ? c.first_slot : 0, w, rho); };
-  const int ra = sm.row0 + rho;
-  const size_t orow = size_t(u.q0 + ra / G) * hq + sm.kvh * G + ra % G;
+  auto prow_of = [&](int i, int rho) {
+    return part_row(c.b0 + i, i == 0 ? c.first_slot : 0, w, rho);
+  };
+  auto out_row = [&](int rho) {
+    const int ra = sm.row0 + rho;
+    return size_t(u.q0 + ra / G) * hq + sm.kvh * G + ra % G;
+  };
   if (nparts <= kFastParts) {
-    // every load issued at once: one memory round trip
-    floatx4 ml[kFastParts];  // reference max, sum, rounded sum
-    floatx4 po[kFastParts];
+    // every load of both rows issued at once: one memory round trip
+    floatx4 ml[NR][kFastParts], po[NR][kFastParts];
 #pragma unroll
-    for (int i = 0; i < kFastParts; ++i) {
-      ml[i] = floatx4{-__builtin_inff(), 0.0f, 0.0f, 0.0f};
-      po[i] = floatx4{0.f, 0.f, 0.f, 0.f};
-      if (i < nparts) {
-        const size_t prow = prow_of(i);
-        ml[i] = *reinterpret_cast<const floatx4*>(ws.part_ml + prow * 4);
-        po[i] = *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
+    for (int k = 0; k < NR; ++k) {
+      const int rho = rho0 + k * kRowSpan;
+#pragma unroll
+      for (int i = 0; i < kFastParts; ++i) {
+        ml[k][i] = floatx4{-__builtin_inff(), 0.0f, 0.0f, 0.0f};
+        po[k][i] = floatx4{0.f, 0.f, 0.f, 0.f};
+        if (i < nparts && rho < sm.rows) {
+          const size_t prow = prow_of(i, rho);
+          ml[k][i] = *reinterpret_cast<const floatx4*>(ws.part_ml + prow * 4);
+          po[k][i] = *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
+        }
       }
     }
-    float M = -__builtin_inff();
 #pragma unroll
-    for (int i = 0; i < kFastParts; ++i) M = fmaxf(M, ml[i][0]);
+    for (int k = 0; k < NR; ++k) {
+      const int rho = rho0 + k * kRowSpan;
+      if (rho >= sm.rows) continue;
+      const size_t orow = out_row(rho);
+      merge_parts<kFastParts>(ml[k], po[k], nparts, out + orow * kD + d4,
+                              lse != nullptr && d4 == 0 ? lse + orow : nullptr);
+    }
+    return;
+  }
+  // more parts: one part at a time, in order
+  for (int k = 0; k < NR; ++k) {
+    const int rho = rho0 + k * kRowSpan;
+    if (rho >= sm.rows) continue;
+    float M = -__builtin_inff();
+    for (int i = 0; i < nparts; ++i) M = fmaxf(M, ws.part_ml[prow_of(i, rho) * 4]);
     float L = 0.0f, Lq = 0.0f;
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
     if (M != -__builtin_inff()) {
-#pragma unroll
-      for (int i = 0; i < kFastParts; ++i) {
-        if (ml[i][0] == -__builtin_inff()) continue;  // absent or empty part
-        const float wgt = __builtin_amdgcn_exp2f(ml[i][0] - M);
-        L += wgt * ml[i][1];
-        Lq += wgt * ml[i][2];
-        acc += wgt * po[i];
+      for (int i = 0; i < nparts; ++i) {
+        const size_t prow = prow_of(i, rho);
+        const floatx4 m = *reinterpret_cast<const floatx4*>(ws.part_ml + prow * 4);
+        if (m[0] == -__builtin_inff()) continue;
+        const float wgt = __builtin_amdgcn_exp2f(m[0] - M);
+        L += wgt * m[1];
+        Lq += wgt * m[2];
+        acc += wgt * *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
       }
     }
+    const size_t orow = out_row(rho);
     const float inv = Lq > 0.0f ? 1.0f / Lq : 0.0f;
     *reinterpret_cast<floatx4*>(out + orow * kD + d4) = acc * inv;
     if (lse != nullptr && d4 == 0) lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
-    return;
   }
-  float M = -__builtin_inff();
-  for (int i = 0; i < nparts; ++i) M = fmaxf(M, ws.part_ml[prow_of(i) * 4]);
-  float L = 0.0f, Lq = 0.0f;
-  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (M != -__builtin_inff()) {
-    for (int i = 0; i < nparts; ++i) {
-      const size_t prow = prow_of(i);
-      const floatx4 ml = *reinterpret_cast<const floatx4*>(ws.part_ml + prow * 4);
-      if (ml[0] == -__builtin_inff()) continue;
-      const float wgt = __builtin_amdgcn_exp2f(ml[0] - M);
-      L += wgt * ml[1];
-      Lq += wgt * ml[2];
-      acc += wgt * *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
-    }
-  }
-  const float inv = Lq > 0.0f ? 1.0f / Lq : 0.0f;
-  *reinterpret_cast<floatx4*>(out + orow * kD + d4) = acc * inv;
-  if (lse != nullptr && d4 == 0) lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
 }
 
 int main_workgroups() { return device_cu_count(); }
