@@ -119,11 +119,29 @@ __device__ __forceinline__ size_t part_row(int b, int slot, int w, int rho) {
   return (size_t(2 * b + slot) * kWaves + w) * kPassRows + rho;
 }
 
+// floor(n / d) for 0 <= n < 2^42 and 0 < d < 2^31, without a 64-bit integer
+// division: the quotient through d's double reciprocal is within one of the
+// floor (the product's error is below 2^-9), and one integer step corrects it.
+struct DivBy {
+  long long d;
+  double inv;
+  __device__ explicit DivBy(long long d_) : d(d_), inv(1.0 / double(d_)) {}
+  __device__ __forceinline__ long long operator()(long long n) const {
+    long long q = static_cast<long long>(double(n) * inv);
+    if (q * d > n) --q;
+    else if ((q + 1) * d <= n) ++q;
+    return q;
+  }
+};
+
 // First tile of workgroup b when T tiles are cut into nw equal ranges (nw <= T).
 __device__ __forceinline__ long long range_lo(long long T, int b, int nw) { return T * b / nw; }
+__device__ __forceinline__ long long range_lo(long long T, int b, const DivBy& by_nw) {
+  return by_nw(T * b);
+}
 // Workgroup whose range holds tile t.
-__device__ __forceinline__ int range_of(long long t, long long T, int nw) {
-  return int(((t + 1) * nw + T - 1) / T) - 1;
+__device__ __forceinline__ int range_of(long long t, long long T, int nw, const DivBy& by_t) {
+  return int(by_t((t + 1) * nw + T - 1)) - 1;
 }
 
 // The rows of stream w of a unit: KV head, first row and row count (rows == 0:
@@ -278,6 +296,7 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
   // workgroups with work: never more than tiles, so that no range is empty
   const int nw = T < nb ? int(T) : nb;
   // pass B: units, the cut units and each workgroup's first unit
+  const DivBy by_t(T > 0 ? T : 1), by_nw(nw > 0 ? nw : 1);
   int unit_run = 0, tile_run = 0, cut_run = 0;
   for (int base = 0; base < R; base += kThreads) {
     RequestShape s;
@@ -299,7 +318,7 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
     int ncut = 0;
     for (int g = 0; g < s.groups; ++g) {
       const long long ts = tb + g * s.tiles, te = ts + s.tiles;
-      if (range_of(ts, T, nw) != range_of(te - 1, T, nw)) ++ncut;
+      if (range_of(ts, T, nw, by_t) != range_of(te - 1, T, nw, by_t)) ++ncut;
     }
     int tot_c;
     const int cb = cut_run + block_exclusive_sum<kThreads>(ncut, s_scan, &tot_c);
@@ -316,7 +335,7 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
       u.passes = s.passes;
       u.rpp = s.rpp;
       u.group = g;
-      const int b0 = range_of(u.tile_start, T, nw), b1 = range_of(u.tile_end - 1, T, nw);
+      const int b0 = range_of(u.tile_start, T, nw, by_t), b1 = range_of(u.tile_end - 1, T, nw, by_t);
       u.cut = b0 != b1;
       u.pad = 0;
       ws.units[ub + g] = u;
@@ -325,13 +344,13 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
         cu.unit = ub + g;
         cu.b0 = b0;
         cu.b1 = b1;
-        cu.first_slot = range_lo(T, b0, nw) < u.tile_start ? 1 : 0;
+        cu.first_slot = range_lo(T, b0, by_nw) < u.tile_start ? 1 : 0;
         cu.u = u;
         ws.cuts[c++] = cu;
       }
       // workgroups whose range starts inside this unit
       int b = b0;
-      if (range_lo(T, b, nw) < u.tile_start) ++b;
+      if (range_lo(T, b, by_nw) < u.tile_start) ++b;
       for (; b <= b1; ++b) ws.wg_unit[b] = ub + g;
     }
     unit_run += tot_u;
