@@ -211,7 +211,11 @@ size_t echo_build_tree_mask_workspace_size(int32_t R, int32_t N, int32_t budget)
  * Slot s of request r, query head h, uses key/value head h / (Hq/Hkv) and
  * sees the request's KV prefix rows [kv_offsets[r], kv_offsets[r+1]) plus
  * the new keys of its local slots j whose tree_mask bit is set.  Logits
- * sm_scale * <q, k> in fp32, softmax, output sum p * v in fp32.
+ * sm_scale * <q, k> in fp32, softmax, output sum p * v accumulated in fp32
+ * with each probability p rounded to bf16 for the product and the output
+ * divided by the sum of those rounded p (an exact convex combination of V
+ * rows, within 2^-9 of the spread of the V values carrying the weight); the
+ * LSE uses the fp32 sum.  NaN inputs give unspecified outputs.
  *   q        [max_rows][Hq][128]  bf16 (slot-indexed, RoPE already applied)
  *   k_new, v_new [max_rows][Hkv][128] bf16 (K/V of the verify slots)
  *   k_cache, v_cache [kv_rows][Hkv][128] bf16, token-major (request r's prefix

@@ -1,5 +1,6 @@
 // Tree-masked grouped-query verification attention (one verification forward
-// over the flattened super-tree).  Three launches:
+// over the flattened super-tree).  Three launches (a paged cache adds
+// attn_pages first, which checks the block tables' page ids):
 //
 //   attn_plan     one workgroup.  A stream is one KV head of one request
 //                 together with a pass over its rows (rows = verify slots x
