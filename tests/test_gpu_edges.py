@@ -208,3 +208,22 @@ def test_empty_requests_and_prefixes():
     _check_all(b)
     b = make_micro_batch(pool, 0, hq=8, hkv=4, p_range=(0, 300))  # budget 0: decode only
     _check_all(b)
+
+
+# (Hq, Hkv): one KV head (every stream of a unit is a pass of the same head),
+# a KV-head count that is not a power of two, and wide GQA groups, so that the
+# 4-stream units of the attention plan straddle heads and passes in every way
+HEAD_LAYOUTS = [(1, 1), (8, 1), (32, 1), (6, 3), (15, 5), (12, 6), (56, 7), (64, 2), (96, 3)]
+
+
+@pytest.mark.parametrize("hq,hkv", HEAD_LAYOUTS)
+def test_head_layouts_every_row(hq, hkv):
+    """Random trees (up to 30 candidates per request, so up to 31 slots and
+    31 * Hq/Hkv rows per head: several row passes) over prefixes of 0-300 keys;
+    every row of the attention output against the oracle."""
+    rng = np.random.default_rng(hq * 100 + hkv)
+    pool = synth.micro_pool(rng, int(rng.integers(3, 24)), 30, p_neg_inf=0.05)
+    N = int(pool["cand_offsets"][-1])
+    b = make_micro_batch(pool, max(1, N * 3 // 4), hq=hq, hkv=hkv, p_range=(0, 300),
+                         seed=hq + hkv)
+    _check_all(b)
