@@ -439,35 +439,52 @@ __device__ __forceinline__ CopyPlan copy_plan(uint32_t row_bytes) {
 // LDS read; completion is awaited explicitly with vmcnt), and M0, which holds
 // the LDS address of such a load, is set once and stepped by 1 KB.  A write of
 // M0 needs one wait state before an LDS load reads it (s_nop 0).  M0 belongs to
-// the compiler and is restored; the steps clobber SCC.
+// the compiler and is restored; the steps clobber SCC.  kNT marks the loads
+// non-temporal (data no other wave of the workgroup reads): streamed with that
+// hint, HBM-bound batches copy 5-8% faster, while data that sibling waves read
+// again must stay cached.
+#define ECHO_DMA_STEP(J, B, POL) \
+  "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %" #J ", %" #B POL "\n\t"
+#define ECHO_DMA_TILE(POL)                                                                      \
+  "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, %10" POL    \
+  "\n\t" ECHO_DMA_STEP(3, 10, POL) ECHO_DMA_STEP(4, 10, POL) ECHO_DMA_STEP(5, 10, POL)        \
+      ECHO_DMA_STEP(6, 10, POL) ECHO_DMA_STEP(7, 10, POL) ECHO_DMA_STEP(8, 10, POL)             \
+          ECHO_DMA_STEP(9, 10, POL) ECHO_DMA_STEP(2, 11, POL) ECHO_DMA_STEP(3, 11, POL)         \
+              ECHO_DMA_STEP(4, 11, POL) ECHO_DMA_STEP(5, 11, POL) ECHO_DMA_STEP(6, 11, POL)     \
+                  ECHO_DMA_STEP(7, 11, POL) ECHO_DMA_STEP(8, 11, POL) ECHO_DMA_STEP(9, 11, POL) \
+                      "s_mov_b32 m0, %0"
+
+template <bool kNT>
 __device__ __forceinline__ void dma_tile(uint32_t lds_stage, uint64_t kbase, uint64_t vbase,
                                          const uint32_t (&off)[8]) {
   const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_stage);
   const uint64_t kb = uniform64(kbase), vb = uniform64(vbase);
   uint32_t saved;
-#define ECHO_DMA_STEP(J, B) \
-  "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %" #J ", %" #B "\n\t"
-  asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, %10\n\t"
-      ECHO_DMA_STEP(3, 10) ECHO_DMA_STEP(4, 10) ECHO_DMA_STEP(5, 10) ECHO_DMA_STEP(6, 10)
-      ECHO_DMA_STEP(7, 10) ECHO_DMA_STEP(8, 10) ECHO_DMA_STEP(9, 10)
-      ECHO_DMA_STEP(2, 11) ECHO_DMA_STEP(3, 11) ECHO_DMA_STEP(4, 11) ECHO_DMA_STEP(5, 11)
-      ECHO_DMA_STEP(6, 11) ECHO_DMA_STEP(7, 11) ECHO_DMA_STEP(8, 11) ECHO_DMA_STEP(9, 11)
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "s"(lds), "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "v"(off[4]),
-        "v"(off[5]), "v"(off[6]), "v"(off[7]), "s"(kb), "s"(vb)
-      : "memory", "scc");
-#undef ECHO_DMA_STEP
+  if (kNT) {
+    asm volatile(ECHO_DMA_TILE(" nt")
+                 : "=&s"(saved)
+                 : "s"(lds), "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "v"(off[4]),
+                   "v"(off[5]), "v"(off[6]), "v"(off[7]), "s"(kb), "s"(vb)
+                 : "memory", "scc");
+  } else {
+    asm volatile(ECHO_DMA_TILE("")
+                 : "=&s"(saved)
+                 : "s"(lds), "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "v"(off[4]),
+                   "v"(off[5]), "v"(off[6]), "v"(off[7]), "s"(kb), "s"(vb)
+                 : "memory", "scc");
+  }
 }
+#undef ECHO_DMA_TILE
+#undef ECHO_DMA_STEP
 
 // Copy one K+V tile (tn <= 32 valid key rows, rows row_bytes apart) into the
 // stage at LDS address lds_stage.  Rows >= tn re-read row tn-1 (in bounds); the
 // softmax masks those keys.
+template <bool kNT>
 __device__ __forceinline__ void issue_tile(uint32_t lds_stage, uint64_t kbase, uint64_t vbase,
                                            uint32_t row_bytes, int tn, const CopyPlan& cp) {
   if (tn == kTileKeys) {
-    dma_tile(lds_stage, kbase, vbase, cp.off);
+    dma_tile<kNT>(lds_stage, kbase, vbase, cp.off);
   } else {
     uint32_t off[8];
 #pragma unroll
@@ -476,7 +493,7 @@ __device__ __forceinline__ void issue_tile(uint32_t lds_stage, uint64_t kbase, u
       const int srow = row < tn ? row : tn - 1;
       off[j] = uint32_t(srow) * row_bytes + copy_chunk16(row);
     }
-    dma_tile(lds_stage, kbase, vbase, off);
+    dma_tile<kNT>(lds_stage, kbase, vbase, off);
   }
 }
 
@@ -711,11 +728,23 @@ struct Issuer {
   // prefix row (contiguous cache) or at row 0 of the cache (paged)
   const char *tail_k, *tail_v, *pre_k, *pre_v;
   const int32_t* bt_row;  // paged: the request's block-table row
+  bool nt;                // no other wave of the unit reads this stream's head
 };
 
 // Point the issue side at unit is.ud.
 __device__ __forceinline__ void issuer_unit(Issuer& is, const MainArgs& a, int wid) {
   is.sm = stream_of(is.ud, wid, a.hkv, a.G);
+  // streams of a group are consecutive and head-major: a sibling of the same
+  // head is the previous or the next stream of the group
+  is.nt = true;
+  if (is.ud.passes > 1) {
+    const int passes = is.ud.passes;
+    const int id = kWaves * is.ud.group + wid;
+    const bool prev = wid > 0 && (id - 1) / passes == id / passes;
+    const bool next =
+        wid + 1 < kWaves && id + 1 < a.hkv * passes && (id + 1) / passes == id / passes;
+    is.nt = !(prev || next);
+  }
   const size_t row_bytes = size_t(a.hkv) * kD * 2;
   const size_t head = size_t(is.sm.kvh) * kD * 2;
   is.tail_k = reinterpret_cast<const char*>(a.k_new) + size_t(is.ud.q0) * row_bytes + head;
@@ -764,8 +793,13 @@ __device__ __forceinline__ void issue_next(Issuer& is, const MainArgs& a, const 
       vb = is.pre_v + off;
       tn = min(kTileKeys, is.ud.P - pt * kTileKeys);
     }
-    issue_tile(ring_lds + uint32_t((is.k & 1) * kStageBytes), reinterpret_cast<uint64_t>(kb),
-               reinterpret_cast<uint64_t>(vb), row_bytes, tn, cp);
+    const uint32_t stage = ring_lds + uint32_t((is.k & 1) * kStageBytes);
+    if (is.nt)
+      issue_tile<true>(stage, reinterpret_cast<uint64_t>(kb), reinterpret_cast<uint64_t>(vb),
+                       row_bytes, tn, cp);
+    else
+      issue_tile<false>(stage, reinterpret_cast<uint64_t>(kb), reinterpret_cast<uint64_t>(vb),
+                        row_bytes, tn, cp);
   }
   ++is.k;
 }
