@@ -916,7 +916,9 @@ __device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws,
         float* po = a.out + orow * kD;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt)
-          *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = rt[i].o[dt] * inv;
+          // written once and not read again here: stored with the non-temporal hint
+          __builtin_nontemporal_store(rt[i].o[dt] * inv,
+                                      reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg));
         if (a.lse != nullptr && lg == 0)
           a.lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
       } else {
@@ -1020,7 +1022,7 @@ __device__ __forceinline__ void merge_parts(const floatx4 (&ml)[NP], const float
     }
   }
   const float inv = Lq > 0.0f ? 1.0f / Lq : 0.0f;
-  *reinterpret_cast<floatx4*>(o) = acc * inv;
+  __builtin_nontemporal_store(acc * inv, reinterpret_cast<floatx4*>(o));
   if (l != nullptr) *l = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
 }
 
@@ -1096,7 +1098,7 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv,
     }
     const size_t orow = out_row(rho);
     const float inv = Lq > 0.0f ? 1.0f / Lq : 0.0f;
-    *reinterpret_cast<floatx4*>(out + orow * kD + d4) = acc * inv;
+    __builtin_nontemporal_store(acc * inv, reinterpret_cast<floatx4*>(out + orow * kD + d4));
     if (lse != nullptr && d4 == 0) lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
   }
 }
