@@ -254,3 +254,32 @@ def test_serving_step_with_paged_cache():
                                               page_size, qo1, mask1, cfg.hq, cfg.hkv,
                                               b["sm_scale"])
     gc.compare_attn(out2, lse2, ro, rl, range(cfg.R))
+
+
+@pytest.mark.parametrize("hq,hkv,page_size", [(8, 1, 32), (15, 5, 64), (56, 7, 32), (96, 3, 64)])
+def test_paged_attention_head_layouts(hq, hkv, page_size):
+    """The paged path over unusual head layouts (one KV head, KV-head counts
+    that are not powers of two, GQA up to 32, several row passes per head):
+    bit for bit the contiguous GPU path, and every row against the oracle."""
+    from tests.test_gpu_edges import make_micro_batch, _front_ref
+    rng = np.random.default_rng(hq * 1000 + hkv * 10 + page_size)
+    pool = synth.micro_pool(rng, int(rng.integers(3, 24)), 30, p_neg_inf=0.05)
+    N = int(pool["cand_offsets"][-1])
+    b = make_micro_batch(pool, max(1, N * 3 // 4), hq=hq, hkv=hkv, p_range=(0, 300),
+                         seed=hq + hkv + page_size)
+    ref = _front_ref(b)
+    m = ref["mask"]
+    _log(f"[serve] paged layouts hq={hq} hkv={hkv} page_size={page_size}")
+    kp, vp, bt, plen = to_pages(b["k_cache"], b["v_cache"], b["kv_offsets"], page_size, rng)
+    out, lse, status = run_paged(b, m, kp, vp, bt, plen, page_size)
+    assert status == 0
+    st, res = gc.run_gpu(b, ref["target"])
+    nq = m["num_slots"]
+    assert np.array_equal(out[:nq].view(np.uint32), res["out"][:nq].view(np.uint32))
+    assert np.array_equal(lse[:nq].view(np.uint32), res["lse"][:nq].view(np.uint32))
+    cfg = b["cfg"]
+    rows = list(range(nq))
+    ro, rl, _ = oracle.tree_verify_attn_paged(b["q"], b["k_new"], b["v_new"], kp, vp, bt, plen,
+                                              page_size, m["q_offsets"], m["tree_mask"], cfg.hq,
+                                              cfg.hkv, b["sm_scale"], rows=rows)
+    gc.compare_attn(out, lse, ro, rl, rows)
