@@ -110,6 +110,58 @@ __device__ __forceinline__ uint64_t rank_word(uint32_t key, int i) {
   return (uint64_t(key) << 32) | uint64_t(0xFFFFFFFFu - uint32_t(i));
 }
 
+// Position of this lane among the lanes of `bal` below it.
+__device__ __forceinline__ int lanes_below(uint64_t bal) {
+  return int(__builtin_amdgcn_mbcnt_hi(uint32_t(bal >> 32),
+                                       __builtin_amdgcn_mbcnt_lo(uint32_t(bal), 0u)));
+}
+
+// counter[d] += 1 for every lane with `on` and depth d, with one LDS atomic per
+// distinct depth in the wave; returns the counter's value before this lane's
+// increment (lanes of one depth take consecutive values).  Every lane of the
+// wave must call it.
+__device__ __forceinline__ int add_by_depth(bool on, int d, int* counter) {
+  uint64_t rem = __ballot(on);
+  int before = 0;
+  while (rem != 0ull) {  // uniform: one round per distinct depth
+    const int lead = __builtin_ctzll(rem);
+    const int dl = __shfl(d, lead, kWave);
+    const uint64_t bal = __ballot(on && d == dl);
+    int base = 0;
+    if ((threadIdx.x & (kWave - 1)) == lead) base = atomicAdd(&counter[dl], __popcll(bal));
+    base = __shfl(base, lead, kWave);
+    if (on && d == dl) before = base + lanes_below(bal);
+    rem &= ~bal;
+  }
+  return before;
+}
+
+// Append candidate i (key k) to a depth's appendable list when `take`, with one
+// LDS atomic per wave for the list length and one for the depth's largest key
+// (per-lane atomics on the same two words serialise).  Every lane of the wave
+// must call it (the ballot and shuffles are wave-wide).
+__device__ __forceinline__ void append_wave(bool take, int i, uint32_t k, int* cnt, uint32_t* mx,
+                                            int32_t* list, uint64_t* word) {
+  const uint64_t bal = __ballot(take);
+  if (bal == 0ull) return;  // uniform
+  const int lane = threadIdx.x & (kWave - 1);
+  const int n = __popcll(bal);
+  uint32_t km = take ? k : 0u;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) km = max(km, uint32_t(__shfl_xor(int(km), off, kWave)));
+  int base = 0;
+  if (lane == 0) {
+    base = atomicAdd(cnt, n);
+    atomicMax(mx, km);
+  }
+  base = __shfl(base, 0, kWave);
+  if (take) {
+    const int pos = base + lanes_below(bal);
+    list[pos] = i;
+    word[pos] = rank_word(k, i);
+  }
+}
+
 // Rank of every listed candidate among the A listed ones (key descending,
 // local index ascending: the order of their words); the first `dem` are taken.
 // Every lane of a wave reads the same word at a time (an LDS broadcast).
@@ -194,8 +246,8 @@ __device__ void trajectory_staged(int r, int lo, int n, const GateScoreBufs& sb,
       L.dep[i] = uint8_t(dd[q]);
       L.sel[i] = 0;
       ew.rank[lo + i] = -1;
-      if (kk[q] != 0u) atomicAdd(&L.off[dd[q] + 1], 1);  // finite keys have depth <= 16
     }
+    add_by_depth(i < n && kk[q] != 0u, dd[q] + 1, L.off);  // finite keys have depth <= 16
   }
   __syncthreads();
   if (tid < kWave) {  // inclusive scan of the depth counts (18 entries) in one wave
@@ -208,24 +260,28 @@ __device__ void trajectory_staged(int r, int lo, int n, const GateScoreBufs& sb,
     if (tid <= kSlots) L.off[tid] = v;
   }
   __syncthreads();
-  for (int i = tid; i < n; i += kElThreads) {
-    if (L.key[i] == 0u) continue;
-    const int d = L.dep[i];
-    L.order[L.off[d] + atomicAdd(&L.fill[d], 1)] = uint16_t(i);
+  for (int i0 = 0; i0 < n; i0 += kElThreads) {  // bounds uniform in the workgroup
+    const int i = i0 + tid;
+    const bool on = i < n && L.key[i] != 0u;
+    const int d = on ? int(L.dep[i]) : 0;
+    const int k = add_by_depth(on, d, L.fill);
+    if (on) L.order[L.off[d] + k] = uint16_t(i);
   }
   __syncthreads();
   int t = kNone;
   int par = 0;
   for (int d = 1; d <= ECHO_MAX_DEPTH; ++d) {
-    for (int j = L.off[d] + tid; j < L.off[d + 1]; j += kElThreads) {
-      const int i = L.order[j];
-      const int p = L.par[i];
-      if (p >= 0 && !L.sel[p]) continue;
-      const uint32_t k = L.key[i];
-      const int j2 = atomicAdd(&L.cnt[par], 1);
-      L.list[j2] = i;
-      L.word[j2] = rank_word(k, i);
-      atomicMax(&L.mx[par], k);
+    const int j1 = L.off[d + 1];
+    for (int j0 = L.off[d]; j0 < j1; j0 += kElThreads) {  // bounds uniform in the workgroup
+      const int j = j0 + tid;
+      int i = 0;
+      bool take = false;
+      if (j < j1) {
+        i = L.order[j];
+        const int p = L.par[i];
+        take = p < 0 || L.sel[p];
+      }
+      append_wave(take, i, take ? L.key[i] : 0u, &L.cnt[par], &L.mx[par], L.list, L.word);
     }
     __syncthreads();
     const int A = L.cnt[par];
@@ -268,16 +324,16 @@ __device__ void trajectory_global(int r, int lo, int n, const GateScoreBufs& sb,
   int t = kNone;
   int par = 0;
   for (int d = 1; d <= ECHO_MAX_DEPTH; ++d) {
-    for (int i = tid; i < n; i += kElThreads) {
-      if (int(sb.depth[lo + i]) != d) continue;
-      const uint32_t k = sb.keys[lo + i];
-      if (k == 0u) continue;
-      const int p = sb.pglob[lo + i];
-      if (p >= 0 && !sel[p - lo]) continue;
-      const int j2 = atomicAdd(&L.cnt[par], 1);
-      list[j2] = i;
-      word[j2] = rank_word(k, i);
-      atomicMax(&L.mx[par], k);
+    for (int i0 = 0; i0 < n; i0 += kElThreads) {  // bounds uniform in the workgroup
+      const int i = i0 + tid;
+      uint32_t k = 0u;
+      bool take = false;
+      if (i < n && int(sb.depth[lo + i]) == d) {
+        k = sb.keys[lo + i];
+        const int p = sb.pglob[lo + i];
+        take = k != 0u && (p < 0 || sel[p - lo]);
+      }
+      append_wave(take, i, k, &L.cnt[par], &L.mx[par], list, word);
     }
     __syncthreads();
     const int A = L.cnt[par];
