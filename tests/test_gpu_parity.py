@@ -57,7 +57,7 @@ def test_presets_match_oracle(name, seed):
     _log(f"[parity] {name} seed={seed}: ok, attention max abs {err[0]:.2e}, row rel {err[1]:.2e}")
 
 
-@pytest.mark.parametrize("name", ["tiny", "l8b"])
+@pytest.mark.parametrize("name", ["tiny", "l8b", "l70b", "q235b", "long"])
 def test_peaked_queries(name):
     """Queries scaled x4: sharper softmax, outputs of order one."""
     b = synth.make_batch(name, 7, q_scale=4.0)
