@@ -84,14 +84,20 @@ def attn_source_hash():
     return h.hexdigest()
 
 
-def traffic_from_profile(attn_src_hash):
-    """HBM bytes per attention-kernel launch from the committed rocprofv3 PMC summary."""
-    path = os.path.join(ROOT, "profiles", "attn_main_q235b_pmc.json")
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "attn_main_q235b_pmc.json")
+
+
+def traffic_from_profile(attn_src_hash, workload_key, path=PMC_SUMMARY):
+    """HBM bytes per attention-kernel launch from the committed rocprofv3 PMC summary.
+
+    None unless the counters were taken on this workload (config, seed, gate policy, KV
+    layout, serving step) with the current attention source and build flags.
+    """
     if not os.path.exists(path):
         return None
     with open(path) as f:
         d = json.load(f)
-    if d.get("attn_src_sha256") != attn_src_hash:
+    if d.get("attn_src_sha256") != attn_src_hash or d.get("workload_key") != workload_key:
         return None
     return d.get("hbm_bytes_per_launch")
 
@@ -293,7 +299,9 @@ def main():
     value = nq / (ms_step / 1000.0)
     bytes_alg, flops_alg = attn_algorithmic(batch, res, cfg)
     achieved_gbs = bytes_alg / (attn_us * 1e-6) / 1e9
-    traffic = traffic_from_profile(attn_source_hash())
+    traffic = traffic_from_profile(attn_source_hash(), {
+        "config": args.config, "seed": args.seed, "gate_policy": args.gate_policy,
+        "page_size": page_size, "serve": bool(args.serve)})
 
     out = {
         "metric": METRIC,
