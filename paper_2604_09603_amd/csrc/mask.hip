@@ -51,28 +51,44 @@ __device__ __forceinline__ uint32_t nonzero_bytes(uint32_t w) {
 
 template <bool kAligned>
 __device__ __forceinline__ Flags load_flags(const uint8_t* __restrict__ sel, int start, int N) {
-  Flags f = {0ull, 0ull};
+  constexpr int kWords = kBytesPerThread / 4;
+  uint32_t w[kWords];
   if (kAligned && start + kBytesPerThread <= N) {
     const uint4* p = reinterpret_cast<const uint4*>(sel + start);
-    uint4 w[8];
 #pragma unroll
-    for (int v = 0; v < 8; ++v) w[v] = p[v];
-#pragma unroll
-    for (int v = 0; v < 8; ++v) {
-      const uint64_t nib = uint64_t(nonzero_bytes(w[v].x)) | (uint64_t(nonzero_bytes(w[v].y)) << 4) |
-                           (uint64_t(nonzero_bytes(w[v].z)) << 8) |
-                           (uint64_t(nonzero_bytes(w[v].w)) << 12);
-      if (v < 4) f.lo |= nib << (16 * v);
-      else f.hi |= nib << (16 * (v - 4));
+    for (int v = 0; v < kWords / 4; ++v) {
+      const uint4 q = p[v];
+      w[4 * v] = q.x;
+      w[4 * v + 1] = q.y;
+      w[4 * v + 2] = q.z;
+      w[4 * v + 3] = q.w;
     }
   } else {
-    for (int b = 0; b < kBytesPerThread; ++b) {
-      const int g = start + b;
-      if (g < N && sel[g] != 0) {
-        if (b < 64) f.lo |= uint64_t(1) << b;
-        else f.hi |= uint64_t(1) << (b - 64);
-      }
+    // the end of the array, or an array that is not 16-byte aligned: single
+    // bytes, every load issued before the first is used (one memory round trip,
+    // not one per byte).  Addresses are clamped into the array (start < N) and
+    // the bytes past its end are dropped afterwards.
+    uint8_t bt[kBytesPerThread];
+#pragma unroll
+    for (int k = 0; k < kBytesPerThread; ++k) bt[k] = sel[min(start + k, N - 1)];
+#pragma unroll
+    for (int v = 0; v < kWords; ++v) {
+      uint32_t x = 0u;
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        x |= (start + 4 * v + k < N ? uint32_t(bt[4 * v + k]) : 0u) << (8 * k);
+      w[v] = x;
     }
+  }
+  Flags f = {0ull, 0ull};
+#pragma unroll
+  for (int v = 0; v < kWords / 4; ++v) {
+    const uint64_t nib = uint64_t(nonzero_bytes(w[4 * v])) |
+                         (uint64_t(nonzero_bytes(w[4 * v + 1])) << 4) |
+                         (uint64_t(nonzero_bytes(w[4 * v + 2])) << 8) |
+                         (uint64_t(nonzero_bytes(w[4 * v + 3])) << 12);
+    if (v < 4) f.lo |= nib << (16 * v);
+    else f.hi |= nib << (16 * (v - 4));
   }
   return f;
 }

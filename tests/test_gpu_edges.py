@@ -227,3 +227,43 @@ def test_head_layouts_every_row(hq, hkv):
     b = make_micro_batch(pool, max(1, N * 3 // 4), hq=hq, hkv=hkv, p_range=(0, 300),
                          seed=hq + hkv)
     _check_all(b)
+
+
+@pytest.mark.parametrize("name,offset", [("tiny", 1), ("tiny", 3), ("l8b", 1), ("l8b", 2)])
+def test_mask_from_unaligned_selection(name, offset):
+    """The packed mask of a selection array that starts off a 16-byte boundary (the
+    byte-wise load path) and, for tiny, ends inside a 128-byte chunk: every output equal
+    to the oracle's."""
+    import torch
+    import paper_2604_09603_amd as pkg
+    b = synth.make_batch(name, 3)
+    cfg = b["cfg"]
+    g = oracle.gate(b["cand_offsets"], b["parent"], b["logq"], cfg.budget)
+    m = oracle.build_tree_mask(b["cand_offsets"], b["parent"], b["token"], g["selected"],
+                               b["root_token"], b["prefix_len"], cfg.budget, cfg.mask_words)
+    R, N, B, W = cfg.R, int(b["cand_offsets"][-1]), cfg.budget, cfg.mask_words
+    print(f"[edges] unaligned selection {name} offset {offset} N={N}", flush=True)
+    d = torch.device("cuda:0")
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(d)
+    raw = torch.zeros(N + 64, dtype=torch.uint8, device=d)
+    sel = raw[offset:offset + N]
+    sel.copy_(dev(g["selected"].astype(np.uint8)))
+    assert sel.data_ptr() % 16 != 0
+    cap = R + B
+    i32 = lambda n: torch.full((n,), -7, dtype=torch.int32, device=d)
+    q_offsets, slot_cand, slot_parent, slot_token, pos = i32(R + 1), i32(cap), i32(cap), i32(cap), i32(cap)
+    tree_mask = torch.zeros(cap * W, dtype=torch.int32, device=d)
+    status = torch.zeros(1, dtype=torch.int32, device=d)
+    pkg.echo_build_tree_mask(dev(b["cand_offsets"]), dev(b["parent"]), dev(b["token"]), sel,
+                             dev(b["root_token"]), dev(b["prefix_len"]), R, N, B, q_offsets,
+                             slot_cand, slot_parent, slot_token, pos, tree_mask, W, status=status)
+    torch.cuda.synchronize()
+    ns = int(m["num_slots"])
+    assert np.array_equal(q_offsets.cpu().numpy(), m["q_offsets"])
+    assert np.array_equal(slot_cand.cpu().numpy()[:ns], m["slot_cand"][:ns])
+    assert np.array_equal(slot_parent.cpu().numpy()[:ns], m["slot_parent"][:ns])
+    assert np.array_equal(slot_token.cpu().numpy()[:ns], m["slot_token"][:ns])
+    assert np.array_equal(pos.cpu().numpy()[:ns], m["position_ids"][:ns])
+    tm = tree_mask.cpu().numpy().view(np.uint32).reshape(cap, W)
+    assert np.array_equal(tm[:ns], np.asarray(m["tree_mask"]).reshape(-1, W)[:ns].view(np.uint32))
+    assert int(status.cpu()[0]) == int(m["status"])
