@@ -152,9 +152,27 @@ __global__ __launch_bounds__(kGateThreads) void gate_score_kernel(
   const int wstart = max(0, g0 - kWinBack);
   const int wlen = min(N, g0 + kGateThreads) - wstart;
 
-  for (int i = threadIdx.x; i < wlen; i += kGateThreads) {
-    s_par[i] = parent[wstart + i];
-    s_lq[i] = logq[wstart + i];
+  if (wlen > 0) {  // N = 0 still launches one block, with nothing to read
+    // every load of the window issued before the first is stored (one memory
+    // round trip); addresses are clamped into the window
+    constexpr int kWinLoads = kWin / kGateThreads;
+    static_assert(kWin % kGateThreads == 0, "window tiling");
+    int32_t vp[kWinLoads];
+    float vl[kWinLoads];
+#pragma unroll
+    for (int k = 0; k < kWinLoads; ++k) {
+      const int a = wstart + min(int(threadIdx.x) + k * kGateThreads, wlen - 1);
+      vp[k] = parent[a];
+      vl[k] = logq[a];
+    }
+#pragma unroll
+    for (int k = 0; k < kWinLoads; ++k) {
+      const int i = int(threadIdx.x) + k * kGateThreads;
+      if (i < wlen) {
+        s_par[i] = vp[k];
+        s_lq[i] = vl[k];
+      }
+    }
   }
   for (int i = threadIdx.x; i <= R; i += kGateThreads) s_offs[i] = cand_offsets[i];
   for (int i = threadIdx.x; i < kHistBins; i += kGateThreads) s_hist[i] = 0u;
