@@ -208,6 +208,13 @@ def test_empty_requests_and_prefixes():
     _check_all(b)
     b = make_micro_batch(pool, 0, hq=8, hkv=4, p_range=(0, 300))  # budget 0: decode only
     _check_all(b)
+    # no candidates in the whole batch (N = 0): every request verifies its root only
+    empty = dict(cand_offsets=np.zeros(4, np.int32), parent=np.zeros(0, np.int32),
+                 token=np.zeros(0, np.int32), logq=np.zeros(0, np.float32),
+                 root_token=np.array([1, 2, 3], np.int32))
+    b = make_micro_batch(empty, 4, hq=8, hkv=4, p_range=(0, 50))
+    res, _ = _check_all(b)
+    assert res["num_slots"] == 3
 
 
 # (Hq, Hkv): one KV head (every stream of a unit is a pass of the same head),
