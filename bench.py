@@ -291,6 +291,26 @@ def main():
     pkg.set_attn_profile_events(None, None)
     attn_ms = [a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]
     attn_us = 1000.0 * float(np.mean(attn_ms))
+    # 3. per-stage times: an event pair around each call of the step, in a pass of
+    # its own (the event packets add idle time, so the stages sum to more than a step)
+    stages = [("gate", st.gate), ("mask", st.mask), ("attn", st.attn), ("accept", st.accept)]
+    if args.serve:
+        stages.append(("commit", st.commit))
+    n_stage = min(args.steps, 20)
+    stage_ev = {name: [] for name, _ in stages}
+    torch.cuda.synchronize()
+    for _ in range(n_stage):
+        for name, fn in stages:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            stage_ev[name].append((a, b))
+        if args.serve:  # as in a step: the next one repeats this one
+            st.cached_len.copy_(st.prefix_len, non_blocking=True)
+    torch.cuda.synchronize()
+    stage_us = {name: 1000.0 * float(np.mean([a.elapsed_time(b) for a, b in evs]))
+                for name, evs in stage_ev.items()}
 
     res = st.fetch()
     if res["status"] != 0:
@@ -339,6 +359,10 @@ def main():
             "tflops": flops_alg / (attn_us * 1e-6) / 1e12,
             "mfma_frac": flops_alg / (attn_us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS,
         },
+        "draft_nodes_per_sec": int(res["num_selected"]) / (ms_step / 1000.0),
+        "kv_stream_gbs": 4 * cfg.hkv * cfg.head_dim * int(batch["prefix_len"].astype(np.int64).sum())
+                         / (attn_us * 1e-6) / 1e9,
+        "stage_us": stage_us,
         "wall_s_timed": wall,
         "mean_accept_len": float(np.mean(res["accept_len"])),
     }
