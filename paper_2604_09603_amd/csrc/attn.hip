@@ -1077,29 +1077,69 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv,
     }
     return;
   }
-  // more parts: one part at a time, in order
+  // more parts: kFastParts at a time for both rows, in order (the same arithmetic
+  // as the fast path; two memory round trips per batch instead of two per part)
+  float M[NR], L[NR], Lq[NR];
+  floatx4 acc[NR];
+#pragma unroll
+  for (int k = 0; k < NR; ++k) {
+    M[k] = -__builtin_inff();
+    L[k] = 0.0f;
+    Lq[k] = 0.0f;
+    acc[k] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int i0 = 0; i0 < nparts; i0 += kFastParts) {
+    float mb[NR][kFastParts];
+#pragma unroll
+    for (int k = 0; k < NR; ++k)
+#pragma unroll
+      for (int j = 0; j < kFastParts; ++j) {
+        const int rho = rho0 + k * kRowSpan;
+        mb[k][j] = i0 + j < nparts && rho < sm.rows ? ws.part_ml[prow_of(i0 + j, rho) * 4]
+                                                    : -__builtin_inff();
+      }
+#pragma unroll
+    for (int k = 0; k < NR; ++k)
+#pragma unroll
+      for (int j = 0; j < kFastParts; ++j) M[k] = fmaxf(M[k], mb[k][j]);
+  }
+  for (int i0 = 0; i0 < nparts; i0 += kFastParts) {
+    floatx4 ml[NR][kFastParts], po[NR][kFastParts];
+#pragma unroll
+    for (int k = 0; k < NR; ++k)
+#pragma unroll
+      for (int j = 0; j < kFastParts; ++j) {
+        const int rho = rho0 + k * kRowSpan;
+        ml[k][j] = floatx4{-__builtin_inff(), 0.0f, 0.0f, 0.0f};
+        po[k][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        if (i0 + j < nparts && rho < sm.rows) {
+          const size_t prow = prow_of(i0 + j, rho);
+          ml[k][j] = *reinterpret_cast<const floatx4*>(ws.part_ml + prow * 4);
+          po[k][j] = *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
+        }
+      }
+#pragma unroll
+    for (int k = 0; k < NR; ++k) {
+      if (M[k] == -__builtin_inff()) continue;
+#pragma unroll
+      for (int j = 0; j < kFastParts; ++j) {
+        if (ml[k][j][0] == -__builtin_inff()) continue;
+        const float wgt = __builtin_amdgcn_exp2f(ml[k][j][0] - M[k]);
+        L[k] += wgt * ml[k][j][1];
+        Lq[k] += wgt * ml[k][j][2];
+        acc[k] += wgt * po[k][j];
+      }
+    }
+  }
+#pragma unroll
   for (int k = 0; k < NR; ++k) {
     const int rho = rho0 + k * kRowSpan;
     if (rho >= sm.rows) continue;
-    float M = -__builtin_inff();
-    for (int i = 0; i < nparts; ++i) M = fmaxf(M, ws.part_ml[prow_of(i, rho) * 4]);
-    float L = 0.0f, Lq = 0.0f;
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-    if (M != -__builtin_inff()) {
-      for (int i = 0; i < nparts; ++i) {
-        const size_t prow = prow_of(i, rho);
-        const floatx4 m = *reinterpret_cast<const floatx4*>(ws.part_ml + prow * 4);
-        if (m[0] == -__builtin_inff()) continue;
-        const float wgt = __builtin_amdgcn_exp2f(m[0] - M);
-        L += wgt * m[1];
-        Lq += wgt * m[2];
-        acc += wgt * *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
-      }
-    }
     const size_t orow = out_row(rho);
-    const float inv = Lq > 0.0f ? 1.0f / Lq : 0.0f;
-    __builtin_nontemporal_store(acc * inv, reinterpret_cast<floatx4*>(out + orow * kD + d4));
-    if (lse != nullptr && d4 == 0) lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
+    const float inv = Lq[k] > 0.0f ? 1.0f / Lq[k] : 0.0f;
+    __builtin_nontemporal_store(acc[k] * inv, reinterpret_cast<floatx4*>(out + orow * kD + d4));
+    if (lse != nullptr && d4 == 0)
+      lse[orow] = L[k] > 0.0f ? (M[k] + log2f(L[k])) * kLn2 : -__builtin_inff();
   }
 }
 
