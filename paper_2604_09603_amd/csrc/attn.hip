@@ -249,6 +249,12 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
   __shared__ int2 s_scan2[kThreads / kWave + 1];
   __shared__ uint8_t s_ok[ECHO_MAX_REQUESTS + 1];
   const int tid = threadIdx.x;
+  // one request per thread (R <= 256, the usual case): shapes and their scans
+  // are computed once and kept for pass B; the shape is taken with the same
+  // loads as the validity check
+  const bool single = R <= kThreads;
+  RequestShape s1 = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+  int ub1 = 0, tb1 = 0;
   int bits = 0;
   for (int r = tid; r < R; r += kThreads) {
     bool ok = request_ok(q_offsets, kv, max_rows, r);
@@ -256,19 +262,16 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
       for (int c = 0; c < kv.page_chunks; ++c) ok = ok && kv.page_bad[size_t(r) * kv.page_chunks + c] == 0;
     s_ok[r] = ok ? 1 : 0;
     if (!ok) bits |= ECHO_DATA_BAD_OFFSETS;
+    if (single) s1 = request_shape(q_offsets, kv, ok, R, hkv, G, r);
   }
   __syncthreads();
   auto ok_of = [&](int r) { return r < R && s_ok[r] != 0; };
-  // one request per thread (R <= 256, the usual case): shapes and their scans
-  // are computed once and kept for pass B
-  const bool single = R <= kThreads;
-  RequestShape s1 = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-  int ub1 = 0, tb1 = 0;
 
   // pass A: total units and tiles
   long long T = 0, U = 0;
   for (int base = 0; base < R; base += kThreads) {
-    const RequestShape s = request_shape(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
+    const RequestShape s =
+        single ? s1 : request_shape(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
     int tot_u, tot_t;
     const int2 ex = block_exclusive_sum2<kThreads>(make_int2(s.groups, s.groups * s.tiles), s_scan2,
                                                    &tot_u, &tot_t);
