@@ -213,9 +213,12 @@ size_t echo_build_tree_mask_workspace_size(int32_t R, int32_t N, int32_t budget)
  * the new keys of its local slots j whose tree_mask bit is set.  Logits
  * sm_scale * <q, k> in fp32, softmax, output sum p * v accumulated in fp32
  * with each probability p rounded to bf16 for the product and the output
- * divided by the sum of those rounded p (an exact convex combination of V
- * rows, within 2^-9 of the spread of the V values carrying the weight); the
- * LSE uses the fp32 sum.  NaN inputs give unspecified outputs.
+ * divided by the sum of the weights used (an exact convex combination of V
+ * rows).  Where one key of a 32-key tile may carry more than 1/16 of a row's
+ * weight so far, the bf16 residual p - bf16(p) enters a second product, so
+ * that rows whose weight sits on a few keys keep 2^-17 of relative error on
+ * those weights; elsewhere each weight is within 2^-9 of itself.  The LSE
+ * uses the fp32 sum.  NaN inputs give unspecified outputs.
  *   q        [max_rows][Hq][128]  bf16 (slot-indexed, RoPE already applied)
  *   k_new, v_new [max_rows][Hkv][128] bf16 (K/V of the verify slots)
  *   k_cache, v_cache [kv_rows][Hkv][128] bf16, token-major (request r's prefix
@@ -224,6 +227,9 @@ size_t echo_build_tree_mask_workspace_size(int32_t R, int32_t N, int32_t budget)
  *   out      [max_rows][Hq][128]  float
  *   lse      [max_rows][Hq]       float (nullable), natural log; -inf with out = 0
  *                                 for a row that sees no key
+ *   sm_scale                      finite and > 0 (else ECHO_ERR_INVALID_ARG): the
+ *                                 softmax takes each row's largest raw logit as
+ *                                 its reference before scaling
  * Requests with decreasing offsets, q_offsets beyond max_rows or kv_offsets
  * outside [0, kv_rows] are skipped (ECHO_DATA_BAD_OFFSETS); their rows are
  * not written.  Deterministic: no floating-point atomics.
@@ -325,13 +331,53 @@ int32_t echo_commit_kv(const int32_t* q_offsets, const int32_t* accept_len,
                        int32_t* prefix_len, int32_t* status, echo_stream_t stream);
 
 /*
- * echo_set_attn_profile_events -- measurement hook (not a step of the method).
- * While both events (hipEvent_t) are non-null, every echo_tree_verify_attn
- * call records `start` on its stream right before its main attention kernel
- * and `stop` right after it, so that a harness can time that kernel alone.
- * NULL, NULL switches it off.  Process-wide setting, not thread-safe.
+ * echo_tree_verify_attn_timed, echo_tree_verify_attn_paged_timed -- the two
+ * attention calls above with a measurement of their main kernel (not a step
+ * of the method).  `ev_start` and `ev_stop` (hipEvent_t, both non-null,
+ * created by the caller) are recorded on `stream` right before and right
+ * after the main attention kernel of this call only, so that a harness can
+ * time that kernel alone.  The event packets leave a few microseconds of idle
+ * time around the kernel: a step timed for throughput uses the untimed calls.
+ * Every other argument, output and error is that of the untimed call; null
+ * events give ECHO_ERR_INVALID_ARG.
  */
-int32_t echo_set_attn_profile_events(void* start, void* stop);
+int32_t echo_tree_verify_attn_timed(const uint16_t* q, const uint16_t* k_new,
+                                    const uint16_t* v_new, const uint16_t* k_cache,
+                                    const uint16_t* v_cache, const int64_t* kv_offsets,
+                                    int64_t kv_rows, const int32_t* q_offsets,
+                                    const uint32_t* tree_mask, int32_t mask_words, int32_t R,
+                                    int32_t max_rows, int32_t num_q_heads, int32_t num_kv_heads,
+                                    int32_t head_dim, float sm_scale, float* out, float* lse,
+                                    void* workspace, size_t workspace_bytes, int32_t* status,
+                                    void* ev_start, void* ev_stop, echo_stream_t stream);
+int32_t echo_tree_verify_attn_paged_timed(
+    const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new, const uint16_t* k_pages,
+    const uint16_t* v_pages, int64_t num_pages, int32_t page_size, const int32_t* block_table,
+    int32_t max_pages_per_request, const int32_t* prefix_len, const int32_t* q_offsets,
+    const uint32_t* tree_mask, int32_t mask_words, int32_t R, int32_t max_rows,
+    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, float sm_scale, float* out,
+    float* lse, void* workspace, size_t workspace_bytes, int32_t* status, void* ev_start,
+    void* ev_stop, echo_stream_t stream);
+
+/*
+ * echo_probe_stream_read -- measurement helper (not a step of the method): the
+ * streaming-read ceiling that the verification attention's roofline is read
+ * against.  Reads k and v, each [rows][heads][128] bf16 (a token-major KV
+ * cache), once and writes nothing but, in the unlikely case that the folded
+ * data equals a fixed word, sink[0].
+ *   mode 0  plain 16-byte vector loads, one workgroup per CU over contiguous
+ *           byte ranges
+ *   mode 1  the attention's copy pattern: 32-row tiles, each wave of a
+ *           four-wave workgroup copying one head's 256-byte slices of the
+ *           tile's rows into LDS with direct-to-LDS loads (heads % 4 == 0,
+ *           else ECHO_ERR_UNSUPPORTED; a final partial tile is not read)
+ *   mode 2  the same copies with every wave streaming its own contiguous
+ *           range of 8 KB blocks (rows * heads % 32 == 0, else
+ *           ECHO_ERR_UNSUPPORTED)
+ * k, v 16-byte aligned; rows * heads * 256 < 2^40.
+ */
+int32_t echo_probe_stream_read(const uint16_t* k, const uint16_t* v, int64_t rows, int32_t heads,
+                               int32_t mode, uint32_t* sink, echo_stream_t stream);
 
 const char* echo_status_string(int32_t code);
 const char* echo_version(void);

@@ -37,7 +37,8 @@ EXPORTS = [
     "echo_build_tree_mask", "echo_build_tree_mask_workspace_size",
     "echo_tree_verify_attn", "echo_tree_verify_attn_workspace_size",
     "echo_tree_verify_attn_paged", "echo_accept_logits", "echo_commit_kv",
-    "echo_accept", "echo_set_attn_profile_events", "echo_status_string", "echo_version",
+    "echo_accept", "echo_tree_verify_attn_timed", "echo_tree_verify_attn_paged_timed",
+    "echo_probe_stream_read", "echo_status_string", "echo_version",
 ]
 
 _lib = None
@@ -71,7 +72,13 @@ _SIGS = {
                                   _P]),
     "echo_commit_kv": (_I32, [_P, _P, _P, _I32, _P, _P, _I32, _I32, _I32, _P, _P, _I64, _I32, _P,
                               _I32, _P, _P, _P]),
-    "echo_set_attn_profile_events": (_I32, [_P, _P]),
+    "echo_tree_verify_attn_timed": (_I32, [_P, _P, _P, _P, _P, _P, _I64, _P, _P, _I32, _I32, _I32,
+                                           _I32, _I32, _I32, _F32, _P, _P, _P, _SZ, _P, _P, _P,
+                                           _P]),
+    "echo_tree_verify_attn_paged_timed": (_I32, [_P, _P, _P, _P, _P, _I64, _I32, _P, _I32, _P, _P,
+                                                 _P, _I32, _I32, _I32, _I32, _I32, _I32, _F32, _P,
+                                                 _P, _P, _SZ, _P, _P, _P, _P]),
+    "echo_probe_stream_read": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P]),
     "echo_status_string": (ctypes.c_char_p, [_I32]),
     "echo_version": (ctypes.c_char_p, []),
 }
@@ -119,10 +126,18 @@ def _check(code: int, what: str):
         raise EchoError(f"{what}: {load().echo_status_string(code).decode()} ({code})")
 
 
-def set_attn_profile_events(start=None, stop=None):
-    """Measurement hook: record torch.cuda.Event objects around the main attention kernel."""
-    p = lambda e: None if e is None else ctypes.c_void_p(e.cuda_event)
-    _check(load().echo_set_attn_profile_events(p(start), p(stop)), "echo_set_attn_profile_events")
+def _event(e):
+    return ctypes.c_void_p(e.cuda_event)
+
+
+def echo_probe_stream_read(k, v, rows, heads, mode, sink, stream=None, check=True):
+    """Measurement helper: read two [rows, heads, 128] bf16 tensors once (mode 0: plain
+    vector loads; mode 1: the attention's tile copies into LDS)."""
+    code = load().echo_probe_stream_read(_ptr(k), _ptr(v), int(rows), int(heads), int(mode),
+                                         _ptr(sink), _stream(stream))
+    if check:
+        _check(code, "echo_probe_stream_read")
+    return code
 
 
 def version() -> str:
@@ -234,6 +249,23 @@ def echo_tree_verify_attn(q, k_new, v_new, k_cache, v_cache, kv_offsets, kv_rows
     return code
 
 
+def echo_tree_verify_attn_timed(q, k_new, v_new, k_cache, v_cache, kv_offsets, kv_rows, q_offsets,
+                                tree_mask, mask_words, R, max_rows, hq, hkv, head_dim, sm_scale,
+                                out, lse, workspace, ev_start, ev_stop, status=None, stream=None,
+                                check=True):
+    """echo_tree_verify_attn with two torch.cuda.Event objects recorded around its
+    main kernel on its stream (measurement only)."""
+    code = load().echo_tree_verify_attn_timed(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(kv_offsets),
+        int(kv_rows), _ptr(q_offsets), _ptr(tree_mask), mask_words, R, max_rows, hq, hkv, head_dim,
+        float(sm_scale), _ptr(out), _ptr(lse), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(status), _event(ev_start),
+        _event(ev_stop), _stream(stream))
+    if check:
+        _check(code, "echo_tree_verify_attn_timed")
+    return code
+
+
 def echo_accept(q_offsets, slot_parent, slot_token, target_token, R, max_rows, max_depth,
                 accept_len, accept_slots, bonus_token, status=None, stream=None, check=True):
     """Greedy acceptance of the longest matching path per request."""
@@ -260,6 +292,22 @@ def echo_tree_verify_attn_paged(q, k_new, v_new, k_pages, v_pages, page_size, bl
         _stream(stream))
     if check:
         _check(code, "echo_tree_verify_attn_paged")
+    return code
+
+
+def echo_tree_verify_attn_paged_timed(q, k_new, v_new, k_pages, v_pages, page_size, block_table,
+                                      prefix_len, q_offsets, tree_mask, mask_words, R, max_rows,
+                                      hq, hkv, head_dim, sm_scale, out, lse, workspace, ev_start,
+                                      ev_stop, status=None, stream=None, check=True):
+    """echo_tree_verify_attn_paged with events around its main kernel (measurement only)."""
+    code = load().echo_tree_verify_attn_paged_timed(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pages), _ptr(v_pages), k_pages.shape[0],
+        page_size, _ptr(block_table), block_table.shape[1], _ptr(prefix_len), _ptr(q_offsets),
+        _ptr(tree_mask), mask_words, R, max_rows, hq, hkv, head_dim, sm_scale, _ptr(out),
+        _ptr(lse), _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(status),
+        _event(ev_start), _event(ev_stop), _stream(stream))
+    if check:
+        _check(code, "echo_tree_verify_attn_paged_timed")
     return code
 
 

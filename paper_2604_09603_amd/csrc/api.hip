@@ -9,9 +9,6 @@
 
 namespace echo {
 
-hipEvent_t g_attn_ev_start = nullptr;
-hipEvent_t g_attn_ev_stop = nullptr;
-
 int device_cu_count() {
   static std::mutex mu;
   static std::vector<int> cache;
@@ -33,6 +30,124 @@ int device_cu_count() {
 namespace {
 inline bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
 inline hipStream_t as_stream(echo_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
+
+// The softmax takes each row's maximum of the raw logits as its reference and
+// scales it afterwards, which is only valid for a positive finite scale.
+inline bool scale_ok(float s) { return s > 0.0f && s <= 3.4028234663852886e38f; }
+
+// Host-side checks and argument packing of the contiguous-cache attention.
+int32_t attn_contiguous(const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
+                        const uint16_t* k_cache, const uint16_t* v_cache, const int64_t* kv_offsets,
+                        int64_t kv_rows, const int32_t* q_offsets, const uint32_t* tree_mask,
+                        int32_t mask_words, int32_t R, int32_t max_rows, int32_t num_q_heads,
+                        int32_t num_kv_heads, int32_t head_dim, float sm_scale, float* out,
+                        float* lse, void* workspace, size_t workspace_bytes, int32_t* status,
+                        hipEvent_t ev_start, hipEvent_t ev_stop, hipStream_t stream) {
+  if (R < 1 || max_rows < 0 || num_q_heads < 1 || num_kv_heads < 1 || mask_words < 1 ||
+      kv_rows < 0)
+    return ECHO_ERR_INVALID_ARG;
+  if (num_q_heads % num_kv_heads != 0 || !scale_ok(sm_scale)) return ECHO_ERR_INVALID_ARG;
+  if (head_dim != ECHO_HEAD_DIM || R > ECHO_MAX_REQUESTS || kv_rows >= (int64_t(1) << 31))
+    return ECHO_ERR_UNSUPPORTED;
+  if (int64_t(max_rows) * num_q_heads >= (int64_t(1) << 26)) return ECHO_ERR_UNSUPPORTED;
+  if (!q || !k_new || !v_new || !kv_offsets || !q_offsets || !tree_mask || !out || !workspace)
+    return ECHO_ERR_INVALID_ARG;
+  if (kv_rows > 0 && (!k_cache || !v_cache)) return ECHO_ERR_INVALID_ARG;
+  if ((ev_start == nullptr) != (ev_stop == nullptr)) return ECHO_ERR_INVALID_ARG;
+  if (!aligned256(workspace) ||
+      workspace_bytes < echo::attn_workspace_bytes(R, max_rows, num_q_heads, num_kv_heads))
+    return ECHO_ERR_WORKSPACE;
+  // 16-byte vector loads of every bf16 row
+  const uintptr_t mis = reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k_new) |
+                        reinterpret_cast<uintptr_t>(v_new) | reinterpret_cast<uintptr_t>(k_cache) |
+                        reinterpret_cast<uintptr_t>(v_cache) | reinterpret_cast<uintptr_t>(out);
+  if (mis & 15u) return ECHO_ERR_INVALID_ARG;
+  if (max_rows == 0) return ECHO_OK;
+  echo::AttnArgs a{};
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.kv_offsets = kv_offsets;
+  a.kv_rows = kv_rows;
+  a.q_offsets = q_offsets;
+  a.tree_mask = tree_mask;
+  a.mask_words = mask_words;
+  a.R = R;
+  a.max_rows = max_rows;
+  a.hq = num_q_heads;
+  a.hkv = num_kv_heads;
+  a.sm_scale = sm_scale;
+  a.out = out;
+  a.lse = lse;
+  a.workspace = workspace;
+  a.status = status;
+  a.ev_start = ev_start;
+  a.ev_stop = ev_stop;
+  return echo::launch_tree_verify_attn(a, stream);
+}
+
+// The same for a paged prefix.
+int32_t attn_paged(const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
+                   const uint16_t* k_pages, const uint16_t* v_pages, int64_t num_pages,
+                   int32_t page_size, const int32_t* block_table, int32_t max_pages_per_request,
+                   const int32_t* prefix_len, const int32_t* q_offsets, const uint32_t* tree_mask,
+                   int32_t mask_words, int32_t R, int32_t max_rows, int32_t num_q_heads,
+                   int32_t num_kv_heads, int32_t head_dim, float sm_scale, float* out, float* lse,
+                   void* workspace, size_t workspace_bytes, int32_t* status, hipEvent_t ev_start,
+                   hipEvent_t ev_stop, hipStream_t stream) {
+  if (R < 1 || max_rows < 0 || num_q_heads < 1 || num_kv_heads < 1 || mask_words < 1 ||
+      num_pages < 1 || max_pages_per_request < 1)
+    return ECHO_ERR_INVALID_ARG;
+  if (num_q_heads % num_kv_heads != 0 || !scale_ok(sm_scale)) return ECHO_ERR_INVALID_ARG;
+  // a page holds whole 32-key tiles and a power-of-two number of rows
+  if (page_size < 32 || (page_size & (page_size - 1)) != 0) return ECHO_ERR_UNSUPPORTED;
+  if (head_dim != ECHO_HEAD_DIM || R > ECHO_MAX_REQUESTS) return ECHO_ERR_UNSUPPORTED;
+  if (num_pages * int64_t(page_size) >= (int64_t(1) << 31)) return ECHO_ERR_UNSUPPORTED;
+  if (int64_t(max_pages_per_request) * page_size >= (int64_t(1) << 31)) return ECHO_ERR_UNSUPPORTED;
+  if (int64_t(max_rows) * num_q_heads >= (int64_t(1) << 26)) return ECHO_ERR_UNSUPPORTED;
+  if (!q || !k_new || !v_new || !k_pages || !v_pages || !block_table || !prefix_len ||
+      !q_offsets || !tree_mask || !out || !workspace)
+    return ECHO_ERR_INVALID_ARG;
+  if ((ev_start == nullptr) != (ev_stop == nullptr)) return ECHO_ERR_INVALID_ARG;
+  if (!aligned256(workspace) ||
+      workspace_bytes < echo::attn_workspace_bytes(R, max_rows, num_q_heads, num_kv_heads))
+    return ECHO_ERR_WORKSPACE;
+  const uintptr_t mis = reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k_new) |
+                        reinterpret_cast<uintptr_t>(v_new) | reinterpret_cast<uintptr_t>(k_pages) |
+                        reinterpret_cast<uintptr_t>(v_pages) | reinterpret_cast<uintptr_t>(out);
+  if (mis & 15u) return ECHO_ERR_INVALID_ARG;
+  if (max_rows == 0) return ECHO_OK;
+  echo::AttnArgs a{};
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_cache = k_pages;
+  a.v_cache = v_pages;
+  a.kv_offsets = nullptr;
+  a.kv_rows = 0;
+  a.block_table = block_table;
+  a.prefix_len = prefix_len;
+  a.page_size = page_size;
+  a.max_pages = max_pages_per_request;
+  a.num_pages = num_pages;
+  a.q_offsets = q_offsets;
+  a.tree_mask = tree_mask;
+  a.mask_words = mask_words;
+  a.R = R;
+  a.max_rows = max_rows;
+  a.hq = num_q_heads;
+  a.hkv = num_kv_heads;
+  a.sm_scale = sm_scale;
+  a.out = out;
+  a.lse = lse;
+  a.workspace = workspace;
+  a.status = status;
+  a.ev_start = ev_start;
+  a.ev_stop = ev_stop;
+  return echo::launch_tree_verify_attn(a, stream);
+}
 }  // namespace
 
 extern "C" {
@@ -158,46 +273,27 @@ int32_t echo_tree_verify_attn(const uint16_t* q, const uint16_t* k_new, const ui
                               int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                               float sm_scale, float* out, float* lse, void* workspace,
                               size_t workspace_bytes, int32_t* status, echo_stream_t stream) {
-  if (R < 1 || max_rows < 0 || num_q_heads < 1 || num_kv_heads < 1 || mask_words < 1 ||
-      kv_rows < 0)
-    return ECHO_ERR_INVALID_ARG;
-  if (num_q_heads % num_kv_heads != 0) return ECHO_ERR_INVALID_ARG;
-  if (head_dim != ECHO_HEAD_DIM || R > ECHO_MAX_REQUESTS || kv_rows >= (int64_t(1) << 31))
-    return ECHO_ERR_UNSUPPORTED;
-  if (int64_t(max_rows) * num_q_heads >= (int64_t(1) << 26)) return ECHO_ERR_UNSUPPORTED;
-  if (!q || !k_new || !v_new || !kv_offsets || !q_offsets || !tree_mask || !out || !workspace)
-    return ECHO_ERR_INVALID_ARG;
-  if (kv_rows > 0 && (!k_cache || !v_cache)) return ECHO_ERR_INVALID_ARG;
-  if (!aligned256(workspace) ||
-      workspace_bytes < echo::attn_workspace_bytes(R, max_rows, num_q_heads, num_kv_heads))
-    return ECHO_ERR_WORKSPACE;
-  // 16-byte vector loads of every bf16 row
-  const uintptr_t mis = reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k_new) |
-                        reinterpret_cast<uintptr_t>(v_new) | reinterpret_cast<uintptr_t>(k_cache) |
-                        reinterpret_cast<uintptr_t>(v_cache) | reinterpret_cast<uintptr_t>(out);
-  if (mis & 15u) return ECHO_ERR_INVALID_ARG;
-  if (max_rows == 0) return ECHO_OK;
-  echo::AttnArgs a{};
-  a.q = q;
-  a.k_new = k_new;
-  a.v_new = v_new;
-  a.k_cache = k_cache;
-  a.v_cache = v_cache;
-  a.kv_offsets = kv_offsets;
-  a.kv_rows = kv_rows;
-  a.q_offsets = q_offsets;
-  a.tree_mask = tree_mask;
-  a.mask_words = mask_words;
-  a.R = R;
-  a.max_rows = max_rows;
-  a.hq = num_q_heads;
-  a.hkv = num_kv_heads;
-  a.sm_scale = sm_scale;
-  a.out = out;
-  a.lse = lse;
-  a.workspace = workspace;
-  a.status = status;
-  return echo::launch_tree_verify_attn(a, as_stream(stream));
+  return attn_contiguous(q, k_new, v_new, k_cache, v_cache, kv_offsets, kv_rows, q_offsets,
+                         tree_mask, mask_words, R, max_rows, num_q_heads, num_kv_heads, head_dim,
+                         sm_scale, out, lse, workspace, workspace_bytes, status, nullptr, nullptr,
+                         as_stream(stream));
+}
+
+int32_t echo_tree_verify_attn_timed(const uint16_t* q, const uint16_t* k_new,
+                                    const uint16_t* v_new, const uint16_t* k_cache,
+                                    const uint16_t* v_cache, const int64_t* kv_offsets,
+                                    int64_t kv_rows, const int32_t* q_offsets,
+                                    const uint32_t* tree_mask, int32_t mask_words, int32_t R,
+                                    int32_t max_rows, int32_t num_q_heads, int32_t num_kv_heads,
+                                    int32_t head_dim, float sm_scale, float* out, float* lse,
+                                    void* workspace, size_t workspace_bytes, int32_t* status,
+                                    void* ev_start, void* ev_stop, echo_stream_t stream) {
+  if (ev_start == nullptr || ev_stop == nullptr) return ECHO_ERR_INVALID_ARG;
+  return attn_contiguous(q, k_new, v_new, k_cache, v_cache, kv_offsets, kv_rows, q_offsets,
+                         tree_mask, mask_words, R, max_rows, num_q_heads, num_kv_heads, head_dim,
+                         sm_scale, out, lse, workspace, workspace_bytes, status,
+                         reinterpret_cast<hipEvent_t>(ev_start),
+                         reinterpret_cast<hipEvent_t>(ev_stop), as_stream(stream));
 }
 
 int32_t echo_tree_verify_attn_paged(
@@ -207,53 +303,26 @@ int32_t echo_tree_verify_attn_paged(
     const uint32_t* tree_mask, int32_t mask_words, int32_t R, int32_t max_rows,
     int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, float sm_scale, float* out,
     float* lse, void* workspace, size_t workspace_bytes, int32_t* status, echo_stream_t stream) {
-  if (R < 1 || max_rows < 0 || num_q_heads < 1 || num_kv_heads < 1 || mask_words < 1 ||
-      num_pages < 1 || max_pages_per_request < 1)
-    return ECHO_ERR_INVALID_ARG;
-  if (num_q_heads % num_kv_heads != 0) return ECHO_ERR_INVALID_ARG;
-  // a page holds whole 32-key tiles and a power-of-two number of rows
-  if (page_size < 32 || (page_size & (page_size - 1)) != 0) return ECHO_ERR_UNSUPPORTED;
-  if (head_dim != ECHO_HEAD_DIM || R > ECHO_MAX_REQUESTS) return ECHO_ERR_UNSUPPORTED;
-  if (num_pages * int64_t(page_size) >= (int64_t(1) << 31)) return ECHO_ERR_UNSUPPORTED;
-  if (int64_t(max_pages_per_request) * page_size >= (int64_t(1) << 31)) return ECHO_ERR_UNSUPPORTED;
-  if (int64_t(max_rows) * num_q_heads >= (int64_t(1) << 26)) return ECHO_ERR_UNSUPPORTED;
-  if (!q || !k_new || !v_new || !k_pages || !v_pages || !block_table || !prefix_len ||
-      !q_offsets || !tree_mask || !out || !workspace)
-    return ECHO_ERR_INVALID_ARG;
-  if (!aligned256(workspace) ||
-      workspace_bytes < echo::attn_workspace_bytes(R, max_rows, num_q_heads, num_kv_heads))
-    return ECHO_ERR_WORKSPACE;
-  const uintptr_t mis = reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k_new) |
-                        reinterpret_cast<uintptr_t>(v_new) | reinterpret_cast<uintptr_t>(k_pages) |
-                        reinterpret_cast<uintptr_t>(v_pages) | reinterpret_cast<uintptr_t>(out);
-  if (mis & 15u) return ECHO_ERR_INVALID_ARG;
-  if (max_rows == 0) return ECHO_OK;
-  echo::AttnArgs a{};
-  a.q = q;
-  a.k_new = k_new;
-  a.v_new = v_new;
-  a.k_cache = k_pages;
-  a.v_cache = v_pages;
-  a.kv_offsets = nullptr;
-  a.kv_rows = 0;
-  a.block_table = block_table;
-  a.prefix_len = prefix_len;
-  a.page_size = page_size;
-  a.max_pages = max_pages_per_request;
-  a.num_pages = num_pages;
-  a.q_offsets = q_offsets;
-  a.tree_mask = tree_mask;
-  a.mask_words = mask_words;
-  a.R = R;
-  a.max_rows = max_rows;
-  a.hq = num_q_heads;
-  a.hkv = num_kv_heads;
-  a.sm_scale = sm_scale;
-  a.out = out;
-  a.lse = lse;
-  a.workspace = workspace;
-  a.status = status;
-  return echo::launch_tree_verify_attn(a, as_stream(stream));
+  return attn_paged(q, k_new, v_new, k_pages, v_pages, num_pages, page_size, block_table,
+                    max_pages_per_request, prefix_len, q_offsets, tree_mask, mask_words, R,
+                    max_rows, num_q_heads, num_kv_heads, head_dim, sm_scale, out, lse, workspace,
+                    workspace_bytes, status, nullptr, nullptr, as_stream(stream));
+}
+
+int32_t echo_tree_verify_attn_paged_timed(
+    const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new, const uint16_t* k_pages,
+    const uint16_t* v_pages, int64_t num_pages, int32_t page_size, const int32_t* block_table,
+    int32_t max_pages_per_request, const int32_t* prefix_len, const int32_t* q_offsets,
+    const uint32_t* tree_mask, int32_t mask_words, int32_t R, int32_t max_rows,
+    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, float sm_scale, float* out,
+    float* lse, void* workspace, size_t workspace_bytes, int32_t* status, void* ev_start,
+    void* ev_stop, echo_stream_t stream) {
+  if (ev_start == nullptr || ev_stop == nullptr) return ECHO_ERR_INVALID_ARG;
+  return attn_paged(q, k_new, v_new, k_pages, v_pages, num_pages, page_size, block_table,
+                    max_pages_per_request, prefix_len, q_offsets, tree_mask, mask_words, R,
+                    max_rows, num_q_heads, num_kv_heads, head_dim, sm_scale, out, lse, workspace,
+                    workspace_bytes, status, reinterpret_cast<hipEvent_t>(ev_start),
+                    reinterpret_cast<hipEvent_t>(ev_stop), as_stream(stream));
 }
 
 int32_t echo_accept(const int32_t* q_offsets, const int32_t* slot_parent,
@@ -268,13 +337,6 @@ int32_t echo_accept(const int32_t* q_offsets, const int32_t* slot_parent,
   return echo::launch_accept(q_offsets, slot_parent, slot_token, target_token, R, max_rows,
                              max_depth, accept_len, accept_slots, bonus_token, status,
                              as_stream(stream));
-}
-
-int32_t echo_set_attn_profile_events(void* start, void* stop) {
-  if ((start == nullptr) != (stop == nullptr)) return ECHO_ERR_INVALID_ARG;
-  echo::g_attn_ev_start = reinterpret_cast<hipEvent_t>(start);
-  echo::g_attn_ev_stop = reinterpret_cast<hipEvent_t>(stop);
-  return ECHO_OK;
 }
 
 const char* echo_status_string(int32_t code) {

@@ -51,6 +51,10 @@ constexpr float kLn2 = 0.6931471805599453f;
 // The softmax reference max is raised only when a logit exceeds it by more than
 // 2^8 (in the exponent): probabilities stay <= 256, exact after normalisation.
 constexpr float kRescaleSlack = 8.0f;
+// A tile whose largest probability in a row exceeds this fraction of the
+// lane's running sum also multiplies V by the bf16 residual p - bf16(p) (see
+// compute_tile).
+constexpr float kSplitFrac = 1.0f / 16.0f;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
@@ -665,6 +669,31 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
     // unrounded sum.
     rt[t].lq = add_bf16x2(pk.w, add_bf16x2(pk.z, add_bf16x2(pk.y, add_bf16x2(pk.x, rt[t].lq))));
     pf[t] = as_bf16x8(pk);
+    // Where a few keys carry the row's weight, the rounding of their
+    // probabilities moves the output by up to 2^-9 of the spread of their
+    // values.  A key of this tile has at most 2^(mt - m) of weight; if that can
+    // exceed 1/16 of the lane's running sum (a lower bound of the row's final
+    // sum), the residuals p - bf16(p), rounded to bf16 too, go through a second
+    // product and into the normaliser, leaving 2^-17 of relative error on these
+    // weights.  Long rows over many keys take this path only on their first
+    // tiles and on outliers.
+    const float pmax = __builtin_amdgcn_exp2f(mt - rt[t].m);
+    if (__ballot(pmax > kSplitFrac * rt[t].l) != 0ull) {
+      uint4 pl;
+      const auto res = [](float p, uint32_t hi2, int half) {
+        const uint32_t b = half ? (hi2 & 0xFFFF0000u) : (hi2 << 16);
+        return p - __uint_as_float(b);
+      };
+      pl.x = pack_bf16x2(res(sv[0], pk.x, 0), res(sv[1], pk.x, 1));
+      pl.y = pack_bf16x2(res(sv[2], pk.y, 0), res(sv[3], pk.y, 1));
+      pl.z = pack_bf16x2(res(sv[4], pk.z, 0), res(sv[5], pk.z, 1));
+      pl.w = pack_bf16x2(res(sv[6], pk.w, 0), res(sv[7], pk.w, 1));
+      rt[t].lq = add_bf16x2(pl.w, add_bf16x2(pl.z, add_bf16x2(pl.y, add_bf16x2(pl.x, rt[t].lq))));
+      const bf16x8 plo = as_bf16x8(pl);
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt)
+        rt[t].o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.vf[dt], plo, rt[t].o[dt], 0, 0, 0);
+    }
   }
   // O^T += V^T P^T
 #pragma unroll
@@ -1200,14 +1229,12 @@ int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
   m.scale2 = a.sm_scale * kLog2e;
   m.out = a.out;
   m.lse = a.lse;
-  // the measurement events (if set) travel with the dispatch; they still leave a
-  // few microseconds of idle time around the kernel, so a step timed for
-  // throughput runs without them
-  const bool prof = g_attn_ev_start != nullptr && g_attn_ev_stop != nullptr;
+  // the measurement events (timed entry points only) travel with the dispatch;
+  // they still leave a few microseconds of idle time around the kernel, so a
+  // step timed for throughput runs without them
   void* main_args[] = {&m, &ws};
   if (hipExtLaunchKernel(reinterpret_cast<const void*>(&attn_main_kernel), dim3(unsigned(nb)),
-                         dim3(kWaves * kWave), main_args, 0, stream,
-                         prof ? g_attn_ev_start : nullptr, prof ? g_attn_ev_stop : nullptr,
+                         dim3(kWaves * kWave), main_args, 0, stream, a.ev_start, a.ev_stop,
                          0) != hipSuccess)
     return ECHO_ERR_HIP;
   // cut units number fewer than the main kernel's workgroups

@@ -75,6 +75,10 @@ struct AttnArgs {
   float* lse;
   void* workspace;
   int32_t* status;
+  // measurement only: recorded on the launch stream right before and right
+  // after the main attention kernel (both null, or both set)
+  hipEvent_t ev_start;
+  hipEvent_t ev_stop;
 };
 int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream);
 size_t attn_workspace_bytes(int32_t R, int32_t max_rows, int32_t hq, int32_t hkv);
@@ -99,9 +103,5 @@ int32_t launch_commit_kv(const int32_t* q_offsets, const int32_t* accept_len,
                          int32_t* prefix_len, int32_t* status, hipStream_t stream);
 
 int device_cu_count();
-
-// measurement hook: events recorded around the main attention kernel (may be null)
-extern hipEvent_t g_attn_ev_start;
-extern hipEvent_t g_attn_ev_stop;
 
 }  // namespace echo

@@ -11,8 +11,9 @@ import torch
 
 from . import (HEAD_DIM, MAX_DEPTH, echo_accept, echo_accept_logits, echo_build_tree_mask,
                echo_commit_kv, echo_gate, echo_gate_elastic, echo_gate_sparse,
-               echo_tree_verify_attn, echo_tree_verify_attn_paged, gate_elastic_workspace_size,
-               gate_workspace_size, tree_verify_attn_workspace_size)
+               echo_tree_verify_attn, echo_tree_verify_attn_paged,
+               echo_tree_verify_attn_paged_timed, echo_tree_verify_attn_timed,
+               gate_elastic_workspace_size, gate_workspace_size, tree_verify_attn_workspace_size)
 
 
 def _aligned_workspace(nbytes, device):
@@ -162,19 +163,28 @@ class VerifyStep:
                              self.position_ids, self.tree_mask, self.W, status=self.status,
                              stream=stream)
 
-    def attn(self, stream=None):
+    def attn(self, stream=None, events=None):
+        """``events``: optional (start, stop) torch.cuda.Event pair recorded around the
+        main attention kernel (the timed entry points; measurement only)."""
         if self.page_size is not None:
-            echo_tree_verify_attn_paged(self.q, self.k_new, self.v_new, self.k_pages, self.v_pages,
-                                        self.page_size, self.block_table, self.cached_len,
-                                        self.q_offsets, self.tree_mask, self.W, self.R, self.cap,
-                                        self.hq, self.hkv, self.D, self.sm_scale, self.out,
-                                        self.lse, self.attn_ws, status=self.status, stream=stream)
+            args = (self.q, self.k_new, self.v_new, self.k_pages, self.v_pages, self.page_size,
+                    self.block_table, self.cached_len, self.q_offsets, self.tree_mask, self.W,
+                    self.R, self.cap, self.hq, self.hkv, self.D, self.sm_scale, self.out,
+                    self.lse, self.attn_ws)
+            if events is None:
+                echo_tree_verify_attn_paged(*args, status=self.status, stream=stream)
+            else:
+                echo_tree_verify_attn_paged_timed(*args, events[0], events[1],
+                                                  status=self.status, stream=stream)
             return
-        echo_tree_verify_attn(self.q, self.k_new, self.v_new, self.k_cache, self.v_cache,
-                              self.kv_offsets, self.kv_rows, self.q_offsets, self.tree_mask,
-                              self.W, self.R, self.cap, self.hq, self.hkv, self.D, self.sm_scale,
-                              self.out, self.lse, self.attn_ws, status=self.status,
-                              stream=stream)
+        args = (self.q, self.k_new, self.v_new, self.k_cache, self.v_cache, self.kv_offsets,
+                self.kv_rows, self.q_offsets, self.tree_mask, self.W, self.R, self.cap, self.hq,
+                self.hkv, self.D, self.sm_scale, self.out, self.lse, self.attn_ws)
+        if events is None:
+            echo_tree_verify_attn(*args, status=self.status, stream=stream)
+        else:
+            echo_tree_verify_attn_timed(*args, events[0], events[1], status=self.status,
+                                        stream=stream)
 
     def accept(self, stream=None):
         if self.serve:
@@ -193,10 +203,10 @@ class VerifyStep:
                        self.v_pages, self.page_size, self.block_table, self.cached_len,
                        status=self.status, stream=stream)
 
-    def run(self, stream=None):
+    def run(self, stream=None, attn_events=None):
         self.gate(stream)
         self.mask(stream)
-        self.attn(stream)
+        self.attn(stream, attn_events)
         self.accept(stream)
         if self.serve:
             self.commit(stream)

@@ -156,22 +156,26 @@ def make_trees(cfg: Config, seed: int):
     )
 
 
-def make_attention_inputs(cfg: Config, seed: int, q_scale: float = 1.0):
-    """Prefix lengths, slot-indexed q/k_new/v_new and the token-major KV cache (bf16 bits)."""
+def _scaled(bits: np.ndarray, scale: float) -> np.ndarray:
+    return bits if scale == 1.0 else f32_to_bf16_bits(bf16_bits_to_f32(bits) * np.float32(scale))
+
+
+def make_attention_inputs(cfg: Config, seed: int, q_scale: float = 1.0, v_scale: float = 1.0):
+    """Prefix lengths, slot-indexed q/k_new/v_new and the token-major KV cache (bf16 bits).
+    q_scale / v_scale multiply the queries / the values (new and cached) after the
+    draw, rounded back to bf16."""
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 1, _salt(cfg)])))
     P = rng.integers(cfg.p_lo, cfg.p_hi + 1, size=cfg.R).astype(np.int32)
     kv_offsets = np.zeros(cfg.R + 1, np.int64)
     kv_offsets[1:] = np.cumsum(P.astype(np.int64))
     cap, D = cfg.capacity, cfg.head_dim
     qkv_ss = np.random.SeedSequence([seed, 2, _salt(cfg)]).spawn(5)
-    q = _normal_bf16(qkv_ss[0], cap * cfg.hq * D)
-    if q_scale != 1.0:
-        q = f32_to_bf16_bits(bf16_bits_to_f32(q) * np.float32(q_scale))
+    q = _scaled(_normal_bf16(qkv_ss[0], cap * cfg.hq * D), q_scale)
     k_new = _normal_bf16(qkv_ss[1], cap * cfg.hkv * D)
-    v_new = _normal_bf16(qkv_ss[2], cap * cfg.hkv * D)
+    v_new = _scaled(_normal_bf16(qkv_ss[2], cap * cfg.hkv * D), v_scale)
     T = int(kv_offsets[-1])
     k_cache = _normal_bf16(qkv_ss[3], T * cfg.hkv * D)
-    v_cache = _normal_bf16(qkv_ss[4], T * cfg.hkv * D)
+    v_cache = _scaled(_normal_bf16(qkv_ss[4], T * cfg.hkv * D), v_scale)
     return dict(
         prefix_len=P, kv_offsets=kv_offsets,
         q=q.reshape(cap, cfg.hq, D), k_new=k_new.reshape(cap, cfg.hkv, D),
@@ -181,12 +185,13 @@ def make_attention_inputs(cfg: Config, seed: int, q_scale: float = 1.0):
     )
 
 
-def make_batch(name_or_cfg, seed: int, attention: bool = True, q_scale: float = 1.0):
+def make_batch(name_or_cfg, seed: int, attention: bool = True, q_scale: float = 1.0,
+               v_scale: float = 1.0):
     cfg = CONFIGS[name_or_cfg] if isinstance(name_or_cfg, str) else name_or_cfg
     b = dict(cfg=cfg, seed=seed)
     b.update(make_trees(cfg, seed))
     if attention:
-        b.update(make_attention_inputs(cfg, seed, q_scale))
+        b.update(make_attention_inputs(cfg, seed, q_scale, v_scale))
     return b
 
 

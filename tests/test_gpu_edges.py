@@ -18,12 +18,13 @@ def _need_gpu():
     gc.require_gpu()
 
 
-def _bf16(rng, *shape):
-    return synth.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32))
+def _bf16(rng, *shape, scale=1.0):
+    return synth.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32) * np.float32(scale))
 
 
-def make_micro_batch(pool, budget, hq=8, hkv=2, p_range=(0, 70), seed=0):
-    """Wrap a candidate pool into a full batch with random attention tensors."""
+def make_micro_batch(pool, budget, hq=8, hkv=2, p_range=(0, 70), seed=0, v_scale=1.0):
+    """Wrap a candidate pool into a full batch with random attention tensors
+    (values multiplied by v_scale and rounded back to bf16)."""
     rng = np.random.default_rng(seed)
     R = len(pool["cand_offsets"]) - 1
     cfg = synth.Config("micro", R, 1, 1, 1.0, 8, budget, hq, hkv, 128, p_range[0], p_range[1],
@@ -40,8 +41,8 @@ def make_micro_batch(pool, budget, hq=8, hkv=2, p_range=(0, 70), seed=0):
              target=rng.integers(0, 4, size=N).astype(np.int32),
              root_target=rng.integers(0, 4, size=R).astype(np.int32),
              prefix_len=P, kv_offsets=kvo, q=_bf16(rng, cap, hq, 128),
-             k_new=_bf16(rng, cap, hkv, 128), v_new=_bf16(rng, cap, hkv, 128),
-             k_cache=_bf16(rng, T, hkv, 128), v_cache=_bf16(rng, T, hkv, 128),
+             k_new=_bf16(rng, cap, hkv, 128), v_new=_bf16(rng, cap, hkv, 128, scale=v_scale),
+             k_cache=_bf16(rng, T, hkv, 128), v_cache=_bf16(rng, T, hkv, 128, scale=v_scale),
              sm_scale=np.float32(1 / math.sqrt(128)))
     return b
 
@@ -196,6 +197,26 @@ def test_few_key_rows_every_row(seed):
                                         b["v_cache"], b["kv_offsets"], m["q_offsets"],
                                         m["tree_mask"], cfg.hq, cfg.hkv, b["sm_scale"])
     gc.compare_attn(res["out"], res["lse"], ro, rl, range(m["num_slots"]))
+
+
+@pytest.mark.parametrize("seed", range(2))
+def test_few_key_rows_scaled_values_every_row(seed):
+    """The few-key batches with every value multiplied by 4: the bf16 rounding of
+    the probabilities moves the output by a fraction of the spread of the values
+    that carry the weight, so this is where the absolute 1e-2 bound is tightest."""
+    rng = np.random.default_rng(300 + seed)
+    pool = synth.micro_pool(rng, 1024, 9, p_neg_inf=0.05)
+    b = make_micro_batch(pool, 2000, hq=8, hkv=2, p_range=(0, 40), seed=seed, v_scale=4.0)
+    ref = _front_ref(b)
+    st, res = gc.run_gpu(b, ref["target"])
+    cfg = b["cfg"]
+    m = ref["mask"]
+    ro, rl, _ = oracle.tree_verify_attn(b["q"], b["k_new"], b["v_new"], b["k_cache"],
+                                        b["v_cache"], b["kv_offsets"], m["q_offsets"],
+                                        m["tree_mask"], cfg.hq, cfg.hkv, b["sm_scale"])
+    err = gc.compare_attn(res["out"], res["lse"], ro, rl, range(m["num_slots"]))
+    print(f"[edges] few keys, V x4, seed {seed}: max abs {err[0]:.2e}, row rel {err[1]:.2e}",
+          flush=True)
 
 
 def test_empty_requests_and_prefixes():

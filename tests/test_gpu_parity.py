@@ -36,7 +36,7 @@ def _attn_ref(batch, m, rows):
 
 
 @pytest.mark.parametrize("name,seed", [("tiny", s) for s in range(5)] +
-                         [(n, s) for n in ["l8b", "l70b", "q235b", "long"] for s in (0, 1)])
+                         [(n, s) for n in ["l8b", "l70b", "q235b", "long"] for s in range(5)])
 def test_presets_match_oracle(name, seed):
     _log(f"[parity] {name} seed={seed}: generating")
     b = synth.make_batch(name, seed)
@@ -68,6 +68,24 @@ def test_peaked_queries(name):
     rows = gc.sample_rows(m["q_offsets"], np.random.default_rng(3))
     ro, rl = _attn_ref(b, m, rows)
     gc.compare_attn(res["out"], res["lse"], ro, rl, rows)
+
+
+@pytest.mark.parametrize("name", ["tiny", "l8b", "l70b", "q235b", "long"])
+def test_scaled_values(name):
+    """Values (new and cached) scaled x4, plain and with queries also scaled x4
+    (outputs of order four, weight on fewer keys): sampled rows of every preset,
+    every row for tiny, at the same absolute bounds."""
+    for q_scale in (1.0, 4.0):
+        b = synth.make_batch(name, 11, q_scale=q_scale, v_scale=4.0)
+        ref = gc.oracle_front(b)
+        st, res = gc.run_gpu(b, ref["target"])
+        gc.compare_front(res, ref, int(b["cand_offsets"][-1]))
+        m = ref["mask"]
+        rows = (list(range(m["num_slots"])) if name == "tiny" else
+                gc.sample_rows(m["q_offsets"], np.random.default_rng(5)))
+        ro, rl = _attn_ref(b, m, rows)
+        err = gc.compare_attn(res["out"], res["lse"], ro, rl, rows)
+        _log(f"[parity] {name} V x4, Q x{q_scale:g}: max abs {err[0]:.2e}, row rel {err[1]:.2e}")
 
 
 def test_repeat_is_bit_identical():

@@ -94,3 +94,45 @@ def test_host_side_errors_need_no_gpu():
     assert lib.echo_accept(P(8), P(8), P(8), P(8), 1, 4, 17, P(8), P(8), P(8), None, None) == pkg.ERR_UNSUPPORTED
     assert lib.echo_build_tree_mask(P(8), P(8), P(8), P(8), P(8), P(8), 1, 1, 64, P(8), P(8), P(8),
                                     P(8), P(8), P(8), 1, None, 0, None, None) == pkg.ERR_INVALID_ARG
+
+
+def test_attention_scale_and_timing_events_checked_on_host():
+    """sm_scale must be finite and positive (the softmax takes the largest raw logit
+    of a row as its reference before scaling); the timed entry points need both
+    events; the read probe checks its mode and head count.  All host-side."""
+    if not os.path.exists(pkg.LIB_PATH):
+        pytest.skip("libecho.so not built")
+    lib = pkg.load()
+    P = ctypes.c_void_p
+    ws = lib.echo_tree_verify_attn_workspace_size(1, 4, 8, 8, 128)
+    attn = lambda scale: lib.echo_tree_verify_attn(
+        P(256), P(256), P(256), P(256), P(256), P(256), 10, P(256), P(256), 1, 1, 4, 8, 8, 128,
+        scale, P(256), None, P(256), ws, None, None)
+    paged = lambda scale: lib.echo_tree_verify_attn_paged(
+        P(256), P(256), P(256), P(256), P(256), 8, 64, P(256), 4, P(256), P(256), P(256), 1, 1, 4,
+        8, 8, 128, scale, P(256), None, P(256), ws, None, None)
+    for bad in (0.0, -0.125, float("nan"), float("inf"), -float("inf")):
+        assert attn(bad) == pkg.ERR_INVALID_ARG, bad
+        assert paged(bad) == pkg.ERR_INVALID_ARG, bad
+    timed = lambda a, b: lib.echo_tree_verify_attn_timed(
+        P(256), P(256), P(256), P(256), P(256), P(256), 10, P(256), P(256), 1, 1, 4, 8, 8, 128,
+        0.088, P(256), None, P(256), ws, None, a, b, None)
+    assert timed(None, None) == pkg.ERR_INVALID_ARG
+    assert timed(P(256), None) == pkg.ERR_INVALID_ARG
+    assert timed(None, P(256)) == pkg.ERR_INVALID_ARG
+    ptimed = lambda a, b: lib.echo_tree_verify_attn_paged_timed(
+        P(256), P(256), P(256), P(256), P(256), 8, 64, P(256), 4, P(256), P(256), P(256), 1, 1, 4,
+        8, 8, 128, 0.088, P(256), None, P(256), ws, None, a, b, None)
+    assert ptimed(None, P(256)) == pkg.ERR_INVALID_ARG
+    # the timed calls check their other arguments exactly as the untimed ones
+    timed_bad_scale = lib.echo_tree_verify_attn_timed(
+        P(256), P(256), P(256), P(256), P(256), P(256), 10, P(256), P(256), 1, 1, 4, 8, 8, 128,
+        -1.0, P(256), None, P(256), ws, None, P(256), P(256), None)
+    assert timed_bad_scale == pkg.ERR_INVALID_ARG
+    probe = lambda heads, mode, k=P(256): lib.echo_probe_stream_read(k, P(256), 64, heads, mode,
+                                                                     P(256), None)
+    assert probe(4, 3) == pkg.ERR_INVALID_ARG
+    assert lib.echo_probe_stream_read(P(256), P(256), 7, 1, 2, P(256), None) == pkg.ERR_UNSUPPORTED
+    assert probe(6, 1) == pkg.ERR_UNSUPPORTED
+    assert probe(4, 0, P(264)) == pkg.ERR_INVALID_ARG
+    assert probe(0, 0) == pkg.ERR_INVALID_ARG
