@@ -13,6 +13,7 @@ import argparse
 import hashlib
 import json
 import os
+import platform
 import sys
 import time
 
@@ -102,67 +103,162 @@ def traffic_from_profile(attn_src_hash, workload_key, path=PMC_SUMMARY):
     return d.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(batch, cfg, checkpoints=None, elastic=None, budget_s=12.0):
-    """The oracle as written, single-threaded, on a bounded sample of the workload."""
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo) and the cores this process may use."""
+    name = platform.processor() or "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return name, len(os.sched_getaffinity(0))
+
+
+def _oracle_front(batch, cfg, checkpoints, elastic):
+    """The oracle's gate, mask and accept on the whole batch (single-threaded)."""
     import numpy as np
-    from threadpoolctl import threadpool_limits
 
     import oracle
     import synth
+    if elastic is not None:
+        g = oracle.elastic_schedule(batch["cand_offsets"], batch["parent"], batch["logq"],
+                                    cfg.budget, [d for d, _ in checkpoints],
+                                    np.array([t for _, t in checkpoints], np.float32),
+                                    elastic[0], elastic[1])
+    elif checkpoints is None:
+        g = oracle.gate(batch["cand_offsets"], batch["parent"], batch["logq"], cfg.budget)
+    else:
+        g = oracle.gate_sparse(batch["cand_offsets"], batch["parent"], batch["logq"],
+                               cfg.budget, [d for d, _ in checkpoints],
+                               np.array([t for _, t in checkpoints], np.float32))
+    m = oracle.build_tree_mask(batch["cand_offsets"], batch["parent"], batch["token"],
+                               g["selected"], batch["root_token"], batch["prefix_len"],
+                               cfg.budget, cfg.mask_words)
+    tgt = synth.target_for_slots(batch, m["q_offsets"], m["slot_cand"])
+    oracle.accept(m["q_offsets"], m["slot_parent"], m["slot_token"], tgt, 16)
+    return m
+
+
+def _oracle_attn_requests(batch, cfg, m, reqs, budget_s):
+    """Float64 oracle attention request by request until budget_s seconds are
+    spent; returns (prefix-key work done, seconds, requests done)."""
+    import numpy as np
+
+    import oracle
+    qo = m["q_offsets"]
+    P = batch["prefix_len"].astype(np.int64)
+    n = np.diff(qo)
+    work, spent, done = 0.0, 0.0, 0
+    for r in reqs:
+        t1 = time.perf_counter()
+        oracle.tree_verify_attn(batch["q"], batch["k_new"], batch["v_new"], batch["k_cache"],
+                                batch["v_cache"], batch["kv_offsets"], qo, m["tree_mask"],
+                                cfg.hq, cfg.hkv, batch["sm_scale"],
+                                rows=range(int(qo[r]), int(qo[r + 1])))
+        spent += time.perf_counter() - t1
+        work += float(P[r] * n[r])
+        done += 1
+        if spent >= budget_s:
+            break
+    return work, spent, done
+
+
+# inputs of the forked oracle workers (set before the pool forks, read-only there)
+_WORKER_STATE = {}
+
+
+def _oracle_worker(reqs):
+    """One process of the all-cores leg: its share of the requests, again and again
+    until the time budget is spent; returns (work, seconds, passes, start, end)
+    with start and end on the host's monotonic clock."""
+    from threadpoolctl import threadpool_limits
+    st = _WORKER_STATE
+    work, spent, done = 0.0, 0.0, 0
+    start = time.perf_counter()
+    with threadpool_limits(limits=1):
+        while reqs and spent < st["budget_s"]:
+            w, t, n = _oracle_attn_requests(st["batch"], st["cfg"], st["m"], reqs,
+                                            st["budget_s"] - spent)
+            work, spent, done = work + w, spent + t, done + n
+    return work, spent, done, start, time.perf_counter()
+
+
+def cpu_baseline(batch, cfg, checkpoints=None, elastic=None, budget_s=12.0, par_budget_s=8.0):
+    """The oracle as written, timed on the host on a bounded sample of the workload.
+
+    One-core leg: gate + mask + accept on the whole batch, then float64 attention
+    request by request for about budget_s seconds; the attention time is scaled
+    by prefix-key work to the whole step.  All-cores leg: the same attention
+    spread over one process per usable core (at most 16), each over its share of
+    the requests for about par_budget_s seconds; the aggregate rate is scaled the
+    same way.  Runs before the GPU is touched, so that the workers can fork.
+    """
+    import multiprocessing
+
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    model, usable = cpu_model()
     with threadpool_limits(limits=1):
         t0 = time.perf_counter()
-        if elastic is not None:
-            g = oracle.elastic_schedule(batch["cand_offsets"], batch["parent"], batch["logq"],
-                                        cfg.budget, [d for d, _ in checkpoints],
-                                        np.array([t for _, t in checkpoints], np.float32),
-                                        elastic[0], elastic[1])
-        elif checkpoints is None:
-            g = oracle.gate(batch["cand_offsets"], batch["parent"], batch["logq"], cfg.budget)
-        else:
-            g = oracle.gate_sparse(batch["cand_offsets"], batch["parent"], batch["logq"],
-                                   cfg.budget, [d for d, _ in checkpoints],
-                                   np.array([t for _, t in checkpoints], np.float32))
-        m = oracle.build_tree_mask(batch["cand_offsets"], batch["parent"], batch["token"],
-                                   g["selected"], batch["root_token"], batch["prefix_len"],
-                                   cfg.budget, cfg.mask_words)
-        tgt = synth.target_for_slots(batch, m["q_offsets"], m["slot_cand"])
-        oracle.accept(m["q_offsets"], m["slot_parent"], m["slot_token"], tgt, 16)
+        m = _oracle_front(batch, cfg, checkpoints, elastic)
         t_front = time.perf_counter() - t0
         qo = m["q_offsets"]
         P = batch["prefix_len"].astype(np.int64)
-        n = np.diff(qo)
-        work_all = float((P * n).sum())
+        work_all = float((P * np.diff(qo)).sum())
         order = np.random.default_rng(0).permutation(cfg.R)
-        done_work, t_attn, used = 0.0, 0.0, []
-        for r in order:
-            rows = list(range(int(qo[r]), int(qo[r + 1])))
-            t1 = time.perf_counter()
-            oracle.tree_verify_attn(batch["q"], batch["k_new"], batch["v_new"], batch["k_cache"],
-                                    batch["v_cache"], batch["kv_offsets"], qo, m["tree_mask"],
-                                    cfg.hq, cfg.hkv, batch["sm_scale"], rows=rows)
-            t_attn += time.perf_counter() - t1
-            done_work += float(P[r] * n[r])
-            used.append(int(r))
-            if t_front + t_attn >= budget_s:
-                break
+        w1, t1, n1 = _oracle_attn_requests(batch, cfg, m, order, max(budget_s - t_front, 0.5))
     nq = int(qo[-1])
-    est = t_front + t_attn * work_all / max(done_work, 1.0)
+    est1 = t_front + t1 * work_all / max(w1, 1.0)
+    procs = max(1, min(16, usable, cfg.R))
+    _WORKER_STATE.update(batch=batch, cfg=cfg, m=m, budget_s=par_budget_s)
+    shares = [order[i::procs].tolist() for i in range(procs)]
+    ctx = multiprocessing.get_context("fork")
+    with ctx.Pool(procs) as pool:
+        parts = pool.map(_oracle_worker, shares, chunksize=1)
+    # from the first worker's start to the last one's end (process start-up excluded)
+    wall = max(p[4] for p in parts) - min(p[3] for p in parts)
+    _WORKER_STATE.clear()
+    wp = sum(p[0] for p in parts)
+    np_done = sum(p[2] for p in parts)
+    est_p = t_front + wall * work_all / max(wp, 1.0)
     return {
-        "value": nq / est, "unit": "verified tree nodes/sec", "cores": 1, "kind": "oracle",
-        "sample": (f"oracle gate+mask+accept on the full batch ({t_front:.2f} s) and float64 "
-                   f"attention for {len(used)} of {cfg.R} requests ({t_attn:.2f} s, "
-                   f"{100.0 * done_work / work_all:.1f}% of the prefix-key work), attention time "
-                   f"scaled by prefix-key work to the whole step ({est:.1f} s)"),
+        "value": nq / est1, "unit": "verified tree nodes/sec", "cores": 1, "kind": "oracle",
+        "cpu_model": model, "usable_cores": usable,
+        "all_cores": {"value": nq / est_p, "unit": "verified tree nodes/sec", "cores": procs,
+                      "processes": procs},
+        "sample": (f"one core: oracle gate+mask+accept on the full batch ({t_front:.2f} s) and "
+                   f"float64 attention for {n1} of {cfg.R} requests ({t1:.2f} s, "
+                   f"{100.0 * w1 / work_all:.1f}% of the prefix-key work), attention scaled by "
+                   f"prefix-key work to the whole step ({est1:.1f} s); all cores: the same "
+                   f"attention over {procs} forked processes, each cycling through its share "
+                   f"of the requests: {np_done} request passes, {100.0 * wp / work_all:.1f}% of "
+                   f"the step's prefix-key work, in {wall:.2f} s wall; scaled the same way "
+                   f"({est_p:.2f} s)"),
     }
+
+
+def _pct(xs, q):
+    import numpy as np
+    return float(np.percentile(np.asarray(xs, np.float64), q))
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="q235b")
     ap.add_argument("--seed", type=int, default=3)
+    ap.add_argument("--flush-mb", type=int, default=512,
+                    help="MiB of device memory written, and as many read, between timed steps "
+                         "(excluded from the timing) so that every step starts with the caches "
+                         "holding other, clean data; 0 = back-to-back steps only")
+    ap.add_argument("--protocol-steps", type=int, default=200,
+                    help="cold steps behind the reported percentiles (at least --steps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--gate-policy", default="topb",
                     choices=["topb", "sparse", "dense", "fixed", "elastic"],
@@ -188,9 +284,9 @@ def main():
         sys.exit(2)
 
     import numpy as np
-    import torch
 
     if args.copy_calibration > 0:
+        import torch
         src = torch.empty(args.copy_calibration, dtype=torch.uint8, device="cuda:0")
         dst = torch.empty_like(src)
         src.fill_(1)
@@ -202,20 +298,30 @@ def main():
         return
 
     import synth
-    import paper_2604_09603_amd as pkg
-    from paper_2604_09603_amd.step import VerifyStep
 
     cfg = synth.CONFIGS[args.config]
     log(f"generating {args.config} seed={args.seed}")
     t0 = time.time()
     batch = synth.make_batch(args.config, args.seed)
-    log(f"generated in {time.time() - t0:.1f} s; uploading")
+    log(f"generated in {time.time() - t0:.1f} s")
     elastic = None
     if args.gate_policy == "elastic":
         checkpoints = gate_checkpoints("sparse", args.config, cfg.depth)
         elastic = (2, cfg.branch)
     else:
         checkpoints = gate_checkpoints(args.gate_policy, args.config, cfg.depth)
+    cpu = None
+    if not args.no_cpu_baseline:
+        # before the GPU is touched: the all-cores leg forks worker processes
+        log("timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline(batch, cfg, checkpoints, elastic)
+
+    import torch
+
+    import paper_2604_09603_amd as pkg
+    from paper_2604_09603_amd.step import VerifyStep
+
+    log("uploading")
     page_size = args.page_size or (64 if args.serve else 0)
     st = VerifyStep(batch, device="cuda:0", checkpoints=checkpoints, elastic=elastic,
                     page_size=page_size or None, serve=args.serve)
@@ -235,6 +341,20 @@ def main():
         logits[rows, torch.from_numpy(tgt.astype(np.int64)).to("cuda:0")] = 8.0
         st.set_logits(logits.to(torch.bfloat16))
         del logits
+    flush = flush_src = None
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda:0")
+    if args.flush_mb > 0:
+        # the flush writes one buffer and then streams another one in with the
+        # read probe's allocating copies, so that the caches hold clean lines of
+        # unrelated data.  A write alone leaves up to a MALL's worth of dirty lines
+        # whose write-back then lands inside the next step: head-strided copies
+        # after a 512 MiB write read 4.6 TB/s instead of 6.0, which a serving loop
+        # (weight reads and small activation writes between two attention calls of
+        # a layer) does not see.  That case is reported separately.
+        flush = torch.empty(args.flush_mb << 20, dtype=torch.uint8, device="cuda:0")
+        flush_src = torch.ones(args.flush_mb << 20, dtype=torch.uint8, device="cuda:0")
+        half = flush_src.view(2, -1)
+        flush_rows = half.shape[1] // (4 * 256)
     torch.cuda.synchronize()
 
     log(f"warmup {args.warmup} steps")
@@ -242,6 +362,7 @@ def main():
         st.run()
     torch.cuda.synchronize()
     step_fn = st.run
+    graph = None
     if args.graph:
         graph = torch.cuda.CUDAGraph()
         side = torch.cuda.Stream()
@@ -259,49 +380,93 @@ def main():
         torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
-    # 1. the timed steps: the whole step, nothing else on the stream
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    log(f"timing {args.steps} steps")
-    torch.cuda.synchronize()
+    new_ev = lambda: torch.cuda.Event(enable_timing=True)
+    flush_k = [0]
+
+    def do_flush():
+        if flush is not None:
+            flush_k[0] = (flush_k[0] + 1) & 0xFF
+            flush.fill_(flush_k[0])
+            pkg.echo_probe_stream_read(half[0], half[1], flush_rows, 4, 2, sink)
+
+    def per_step(n, fn, cold):
+        """n steps, one event pair around each; with cold, the flush write runs
+        between the steps, outside the event pairs.  Returns the step times (ms)."""
+        evs = [(new_ev(), new_ev()) for _ in range(n)]
+        torch.cuda.synchronize()
+        for a, b in evs:
+            if cold:
+                do_flush()
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in evs]
+
+    cold = flush is not None
+    # 1. the timed steps (the contract's K steps): cold unless --flush-mb 0
+    log(f"timing {args.steps} {'cold' if cold else 'warm'} steps")
     wall0 = time.perf_counter()
-    t_start.record(stream)
-    for _ in range(args.steps):
-        step_fn()
-    t_end.record(stream)
-    torch.cuda.synchronize()
+    step_ms = per_step(args.steps, step_fn, cold)
     wall = time.perf_counter() - wall0
-    ms_total = t_start.elapsed_time(t_end)
-    ms_step = ms_total / args.steps
-    # 2. the same steps again with HIP events around the main attention kernel,
-    # recorded by the library on its launch stream.  The event packets add a few
-    # microseconds of idle time around that kernel, so this pass gives the
-    # kernel's duration only, not the step time.
-    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    # torch only reads an event it has recorded itself: record each once, the library re-records
-    for e in ev_a + ev_b:
-        e.record(stream)
-    log(f"timing the attention kernel over {args.steps} steps")
+    ms_step = float(np.median(step_ms))
+    n_proto = max(args.protocol_steps, args.steps)
+    proto_ms = step_ms if n_proto == args.steps else per_step(n_proto, step_fn, cold)
+    # 2. warm: back-to-back steps between one event pair, and per step
+    log(f"timing {n_proto} warm steps")
+    ea, eb = new_ev(), new_ev()
     torch.cuda.synchronize()
-    for i in range(args.steps):
-        pkg.set_attn_profile_events(ev_a[i], ev_b[i])
-        st.run()
+    ea.record(stream)
+    for _ in range(n_proto):
+        step_fn()
+    eb.record(stream)
     torch.cuda.synchronize()
-    pkg.set_attn_profile_events(None, None)
-    attn_ms = [a.elapsed_time(b) for a, b in zip(ev_a, ev_b)]
-    attn_us = 1000.0 * float(np.mean(attn_ms))
-    # 3. per-stage times: an event pair around each call of the step, in a pass of
+    warm_mean = ea.elapsed_time(eb) / n_proto
+    warm_ms = per_step(n_proto, step_fn, False)
+    # 3. the main attention kernel alone: events recorded by the library on its
+    # launch stream around that kernel (the timed entry points).  The event
+    # packets add idle time around the kernel, so this pass gives the kernel's
+    # duration only, not the step time.
+    log(f"timing the attention kernel over {n_proto} cold and {n_proto} warm steps")
+    kev_c = [(new_ev(), new_ev()) for _ in range(n_proto)]
+    kev_w = [(new_ev(), new_ev()) for _ in range(n_proto)]
+    # torch reads only an event it has recorded itself: record each once first
+    for a, b in kev_c + kev_w:
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    for evp in kev_c:
+        if cold:
+            do_flush()
+        st.run(attn_events=evp)
+    for evp in kev_w:
+        st.run(attn_events=evp)
+    # the kernel after a write-only flush (dirty lines left in the caches)
+    kev_d = [(new_ev(), new_ev()) for _ in range(min(n_proto, 50) if cold else 0)]
+    for a, b in kev_d:
+        a.record(stream)
+        b.record(stream)
+    for evp in kev_d:
+        flush.fill_(7)
+        st.run(attn_events=evp)
+    torch.cuda.synchronize()
+    kern_c = [a.elapsed_time(b) * 1000.0 for a, b in kev_c]
+    kern_w = [a.elapsed_time(b) * 1000.0 for a, b in kev_w]
+    kern_d = [a.elapsed_time(b) * 1000.0 for a, b in kev_d]
+    attn_us = float(np.mean(kern_c))
+    # 4. per-stage times: an event pair around each call of the step, in a pass of
     # its own (the event packets add idle time, so the stages sum to more than a step)
     stages = [("gate", st.gate), ("mask", st.mask), ("attn", st.attn), ("accept", st.accept)]
     if args.serve:
         stages.append(("commit", st.commit))
-    n_stage = min(args.steps, 20)
+    n_stage = min(n_proto, 50)
     stage_ev = {name: [] for name, _ in stages}
     torch.cuda.synchronize()
     for _ in range(n_stage):
+        if cold:
+            do_flush()
         for name, fn in stages:
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a, b = new_ev(), new_ev()
             a.record(stream)
             fn()
             b.record(stream)
@@ -309,8 +474,26 @@ def main():
         if args.serve:  # as in a step: the next one repeats this one
             st.cached_len.copy_(st.prefix_len, non_blocking=True)
     torch.cuda.synchronize()
-    stage_us = {name: 1000.0 * float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    stage_us = {name: 1000.0 * float(np.median([a.elapsed_time(b) for a, b in evs]))
                 for name, evs in stage_ev.items()}
+    # 5. the streaming-read ceiling over this batch's own KV cache (both probe
+    # modes, each five times after a flush)
+    ceiling = {}
+    for mode, name in ((0, "plain_loads"), (1, "attention_tile_copies")):
+        if mode == 1 and cfg.hkv % 4 != 0:
+            continue
+        rows_read = st.kv_rows - (st.kv_rows % 32 if mode == 1 else 0)
+        ts = []
+        for _ in range(5):
+            do_flush()
+            a, b = new_ev(), new_ev()
+            a.record(stream)
+            pkg.echo_probe_stream_read(st.k_cache, st.v_cache, rows_read, cfg.hkv, mode, sink)
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        nbytes = 2 * rows_read * cfg.hkv * cfg.head_dim * 2
+        ceiling[name] = nbytes / (float(np.median(ts)) * 1e-3) / 1e9
 
     res = st.fetch()
     if res["status"] != 0:
@@ -322,7 +505,13 @@ def main():
     traffic = traffic_from_profile(attn_source_hash(), {
         "config": args.config, "seed": args.seed, "gate_policy": args.gate_policy,
         "page_size": page_size, "serve": bool(args.serve)})
+    kv_bytes = 4 * cfg.hkv * cfg.head_dim * int(batch["prefix_len"].astype(np.int64).sum())
+    stats = lambda xs: {"median": float(np.median(xs)), "p10": _pct(xs, 10), "p90": _pct(xs, 90),
+                        "mean": float(np.mean(xs)), "n": len(xs)}
 
+    timing_extra = {}
+    if kern_d:
+        timing_extra["attn_main_us_after_write_only_flush"] = stats(kern_d)
     out = {
         "metric": METRIC,
         "value": value,
@@ -346,6 +535,18 @@ def main():
             "kv_layout": f"paged, {page_size}-row pages" if page_size else "contiguous",
             "serve_step": bool(args.serve), "hip_graph": bool(args.graph),
         },
+        "timing": {
+            "protocol": (f"value and ms_per_step: median of the {args.steps} timed steps, one "
+                         "event pair each" + (f", with {args.flush_mb} MiB written to device "
+                                              f"memory and another {args.flush_mb} MiB read "
+                                              "between steps (outside the timing)"
+                                              if cold else ", back to back")),
+            "step_ms_cold" if cold else "step_ms_warm_per_step": stats(proto_ms),
+            "step_ms_warm": {"mean_back_to_back": warm_mean, **stats(warm_ms)},
+            "attn_main_us_cold" if cold else "attn_main_us": stats(kern_c),
+            "attn_main_us_warm": stats(kern_w),
+            **timing_extra,
+        },
         "roofline": {
             "kernel": "attn_main_kernel",
             "bound": "hbm",
@@ -356,19 +557,21 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes": bytes_alg,
             "kernel_us": attn_us,
+            "kernel_us_source": ("mean of the cold pass" if cold else "mean") +
+                                " (HIP events on the kernel's launch stream)",
             "tflops": flops_alg / (attn_us * 1e-6) / 1e12,
             "mfma_frac": flops_alg / (attn_us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS,
+            "read_ceiling_gbs": ceiling,
+            "frac_of_read_ceiling": (achieved_gbs / max(ceiling.values())) if ceiling else None,
         },
         "draft_nodes_per_sec": int(res["num_selected"]) / (ms_step / 1000.0),
-        "kv_stream_gbs": 4 * cfg.hkv * cfg.head_dim * int(batch["prefix_len"].astype(np.int64).sum())
-                         / (attn_us * 1e-6) / 1e9,
+        "kv_stream_gbs": kv_bytes / (attn_us * 1e-6) / 1e9,
         "stage_us": stage_us,
         "wall_s_timed": wall,
         "mean_accept_len": float(np.mean(res["accept_len"])),
     }
-    if not args.no_cpu_baseline:
-        log("timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = cpu_baseline(batch, cfg, checkpoints, elastic)
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
 
 
