@@ -375,8 +375,13 @@ __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
 
 // ---------------------------------------------------------------- main ----
 // LDS tile layout: 32 key rows x 256 bytes per tensor, no padding.  The 16-byte
-// chunk c of row r is stored at chunk position c ^ (r & 15), so that 16 rows
-// read at the same logical column fall into 16 different bank groups.
+// chunk c of row r is stored at chunk position c ^ rot(r & 15), rot swapping
+// the two 2-bit halves of the row's low four bits.  Rows 16 apart share a
+// pattern; within 16 consecutive rows every pattern differs, so the K fragment
+// reads (16 rows, one column) fall into 16 different bank groups, and so do
+// the transposed V reads of two 16-lane blocks (8 rows, 4 at a time, of 2
+// consecutive chunks: the rows' low bits select the chunk's high bits and
+// the next two bits its low bits).
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef short shortx4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) shortx4 lds_shortx4_t;
@@ -403,8 +408,10 @@ __device__ __forceinline__ float add_bf16x2(uint32_t w, float acc) {
                                          __builtin_bit_cast(bf16x2, 0x3F803F80u), acc, false);
 }
 
+__device__ __forceinline__ int swz_pattern(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
+
 __device__ __forceinline__ int swz(int row, int chunk) {
-  return row * 256 + ((chunk ^ (row & 15)) << 4);
+  return row * 256 + ((chunk ^ swz_pattern(row)) << 4);
 }
 
 __device__ __forceinline__ uint64_t uniform64(uint64_t x) {
@@ -420,19 +427,26 @@ constexpr int kCopiesPerTile = 16;  // wave instructions of 1 KB (4 key rows) pe
 // its LDS position.
 __device__ __forceinline__ int copy_row(int j) { return j * 4 + ((threadIdx.x & (kWave - 1)) >> 4); }
 __device__ __forceinline__ uint32_t copy_chunk16(int row) {
-  return uint32_t(((threadIdx.x & 15) ^ (row & 15)) * 16);
+  return uint32_t(((threadIdx.x & 15) ^ swz_pattern(row)) * 16);
 }
 
+// Lane offsets of a full tile's copy.  The copies of a full tile go in four
+// groups of four 1 KB loads (K rows 0-15, K rows 16-31, V rows 0-15, V rows
+// 16-31), one LDS base per group; load j of a group adds 1024 j to both its
+// global and its LDS address (the instruction offset applies to both), so the
+// lane offset is the source offset of its chunk minus 1024 j.  Rows 16 apart
+// have the same swizzle, so the second group of a tensor reuses the offsets
+// from a base 16 rows further on.
 struct CopyPlan {
-  uint32_t off[8];  // byte offset from the tile's first key row (full tile)
+  uint32_t off[4];
 };
 
 __device__ __forceinline__ CopyPlan copy_plan(uint32_t row_bytes) {
   CopyPlan cp;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
+  for (int j = 0; j < 4; ++j) {
     const int row = copy_row(j);
-    cp.off[j] = uint32_t(row) * row_bytes + copy_chunk16(row);
+    cp.off[j] = uint32_t(row) * row_bytes + copy_chunk16(row) - 1024u * uint32_t(j);
   }
   return cp;
 }
@@ -461,6 +475,44 @@ __device__ __forceinline__ CopyPlan copy_plan(uint32_t row_bytes) {
                   ECHO_DMA_STEP(7, 11, POL) ECHO_DMA_STEP(8, 11, POL) ECHO_DMA_STEP(9, 11, POL) \
                       "s_mov_b32 m0, %0"
 
+// A full tile: M0 is set once per group of four loads (four writes per tile
+// instead of sixteen); see CopyPlan.  Operands: %1 LDS stage, %2-%5 lane
+// offsets, %6/%7 K at rows 0 and 16, %8/%9 V at rows 0 and 16.
+#define ECHO_DMA_GROUP(B, POL)                                                        \
+  "global_load_lds_dwordx4 %2, %" #B POL "\n\tglobal_load_lds_dwordx4 %3, %" #B     \
+  " offset:1024" POL "\n\tglobal_load_lds_dwordx4 %4, %" #B " offset:2048" POL      \
+  "\n\tglobal_load_lds_dwordx4 %5, %" #B " offset:3072" POL "\n\t"
+#define ECHO_DMA_FULL(POL)                                                            \
+  "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t" ECHO_DMA_GROUP(6, POL)       \
+  "s_add_u32 m0, m0, 0x1000\n\ts_nop 0\n\t" ECHO_DMA_GROUP(7, POL)                   \
+  "s_add_u32 m0, m0, 0x1000\n\ts_nop 0\n\t" ECHO_DMA_GROUP(8, POL)                   \
+  "s_add_u32 m0, m0, 0x1000\n\ts_nop 0\n\t" ECHO_DMA_GROUP(9, POL) "s_mov_b32 m0, %0"
+
+template <bool kNT>
+__device__ __forceinline__ void dma_tile_full(uint32_t lds_stage, uint64_t kbase, uint64_t vbase,
+                                              uint32_t half_bytes, const uint32_t (&off)[4]) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_stage);
+  const uint64_t kb = uniform64(kbase), vb = uniform64(vbase);
+  const uint64_t kb16 = kb + half_bytes, vb16 = vb + half_bytes;
+  uint32_t saved;
+  if (kNT) {
+    asm volatile(ECHO_DMA_FULL(" nt")
+                 : "=&s"(saved)
+                 : "s"(lds), "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "s"(kb),
+                   "s"(kb16), "s"(vb), "s"(vb16)
+                 : "memory", "scc");
+  } else {
+    asm volatile(ECHO_DMA_FULL("")
+                 : "=&s"(saved)
+                 : "s"(lds), "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "s"(kb),
+                   "s"(kb16), "s"(vb), "s"(vb16)
+                 : "memory", "scc");
+  }
+}
+#undef ECHO_DMA_FULL
+#undef ECHO_DMA_GROUP
+
+// A partial tile (rows clamped to the last valid one): one M0 write per load.
 template <bool kNT>
 __device__ __forceinline__ void dma_tile(uint32_t lds_stage, uint64_t kbase, uint64_t vbase,
                                          const uint32_t (&off)[8]) {
@@ -491,7 +543,7 @@ template <bool kNT>
 __device__ __forceinline__ void issue_tile(uint32_t lds_stage, uint64_t kbase, uint64_t vbase,
                                            uint32_t row_bytes, int tn, const CopyPlan& cp) {
   if (tn == kTileKeys) {
-    dma_tile<kNT>(lds_stage, kbase, vbase, cp.off);
+    dma_tile_full<kNT>(lds_stage, kbase, vbase, 16u * row_bytes, cp.off);
   } else {
     uint32_t off[8];
 #pragma unroll

@@ -56,10 +56,24 @@ CONFIGS = {
 
 ORDER = ["tiny", "l8b", "l70b", "q235b", "long"]
 
+# Shape studies beside the five workloads: narrow GQA groups, where a stream
+# has fewer rows than one 16-row matrix tile (G = 1 decode: one row per KV
+# head; G = 2 with about one draft per request).  Small drafted trees (the
+# shape of the attention, not the tree, is what these measure).
+EXTRA_CONFIGS = {
+    "g1_decode": Config("g1_decode", 64, 4, 4, 2.0, 32, 0, 8, 8, 128, 1024, 8192, ("const", 0.7)),
+    "g1_tree": Config("g1_tree", 64, 4, 4, 2.0, 32, 128, 8, 8, 128, 1024, 8192, ("const", 0.7)),
+    "g2_tree": Config("g2_tree", 64, 4, 4, 2.0, 32, 64, 16, 8, 128, 1024, 8192, ("const", 0.7)),
+}
+CONFIGS.update(EXTRA_CONFIGS)
+
 DESCRIPTION = {
     "tiny": "batch 4, tree 4x4 over vocab 32, B=16, 8q/8kv heads, prefix 256",
     "l8b": "Llama-3.1-8B-shaped layer: batch 32, tree 6x8, B=128, 32q/8kv, prefix 512-2048",
     "l70b": "Llama-3.3-70B-shaped layer: batch 64, tree 8x8, B=256, 64q/8kv, prefix 1024-4096",
     "q235b": "Qwen3-235B-A22B-shaped layer: batch 128, tree 8x10, B=256, 64q/4kv, prefix 1024-8192",
     "long": "long context: batch 16, tree 10x6, B=192, 64q/4kv, prefix 16384-32768",
+    "g1_decode": "GQA group 1, decode only: batch 64, B=0, 8q/8kv, prefix 1024-8192",
+    "g1_tree": "GQA group 1: batch 64, tree 4x4, B=128, 8q/8kv, prefix 1024-8192",
+    "g2_tree": "GQA group 2: batch 64, tree 4x4, B=64, 16q/8kv, prefix 1024-8192",
 }

@@ -57,6 +57,22 @@ def test_presets_match_oracle(name, seed):
     _log(f"[parity] {name} seed={seed}: ok, attention max abs {err[0]:.2e}, row rel {err[1]:.2e}")
 
 
+@pytest.mark.parametrize("name", ["g1_decode", "g1_tree", "g2_tree"])
+def test_narrow_groups_match_oracle(name):
+    """GQA groups of one and two query heads (one row per stream in decode):
+    streams with fewer rows than one matrix tile, sampled rows against the oracle."""
+    _log(f"[parity] {name}: generating")
+    b = synth.make_batch(name, 2)
+    ref = gc.oracle_front(b)
+    st, res = gc.run_gpu(b, ref["target"])
+    gc.compare_front(res, ref, int(b["cand_offsets"][-1]))
+    m = ref["mask"]
+    rows = gc.sample_rows(m["q_offsets"], np.random.default_rng(2), n_requests=6, n_extra=64)
+    ro, rl = _attn_ref(b, m, rows)
+    err = gc.compare_attn(res["out"], res["lse"], ro, rl, rows)
+    _log(f"[parity] {name}: ok, attention max abs {err[0]:.2e}, row rel {err[1]:.2e}")
+
+
 @pytest.mark.parametrize("name", ["tiny", "l8b", "l70b", "q235b", "long"])
 def test_peaked_queries(name):
     """Queries scaled x4: sharper softmax, outputs of order one."""
