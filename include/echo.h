@@ -99,6 +99,27 @@ int32_t echo_gate(const int32_t* cand_offsets, const int32_t* parent, const floa
 size_t echo_gate_workspace_size(int32_t R, int32_t N, int32_t budget);
 
 /*
+ * echo_gate_noalloc -- echo_gate without a caller workspace, for callers that
+ * cannot allocate device memory (work under graph capture, serving loops and
+ * harnesses that forbid hipMalloc).  It allocates nothing: the workspace is a
+ * fixed ECHO_GATE_SCRATCH_BYTES array of the library, one copy per device,
+ * held from the first call on a device until the process ends; the caller
+ * still passes every input and output.  Arguments, outputs, clamps and status
+ * bits are echo_gate's.  Sizes whose workspace exceeds the array
+ * (echo_gate_workspace_size(R, N, budget) > ECHO_GATE_SCRATCH_BYTES; every
+ * N <= 262144 fits at any R <= ECHO_MAX_REQUESTS) give ECHO_ERR_UNSUPPORTED
+ * before any runtime call.  Calls on one device share the array, so calls
+ * that overlap on one device (different streams or threads) race and give
+ * undefined selections; serialise them.  The first call on a device looks the
+ * array's device address up (ECHO_ERR_HIP if that fails).
+ */
+#define ECHO_GATE_SCRATCH_BYTES (8u << 20)
+int32_t echo_gate_noalloc(const int32_t* cand_offsets, const int32_t* parent, const float* logq,
+                          int32_t R, int32_t N, int32_t budget, float* path_score,
+                          uint8_t* selected, int32_t* num_selected, int32_t* status,
+                          echo_stream_t stream);
+
+/*
  * echo_gate_sparse -- echo_gate preceded by sparse gating at checkpoint depths
  * (Section 3.2: layer confidence eq. 6, gating signal eq. 7; truncation as in
  * phase 1 of Alg. 1).

@@ -38,8 +38,9 @@ EXPORTS = [
     "echo_tree_verify_attn", "echo_tree_verify_attn_workspace_size",
     "echo_tree_verify_attn_paged", "echo_accept_logits", "echo_commit_kv",
     "echo_accept", "echo_tree_verify_attn_timed", "echo_tree_verify_attn_paged_timed",
-    "echo_probe_stream_read", "echo_status_string", "echo_version",
+    "echo_probe_stream_read", "echo_gate_noalloc", "echo_status_string", "echo_version",
 ]
+GATE_SCRATCH_BYTES = 8 << 20
 
 _lib = None
 
@@ -52,6 +53,7 @@ _F32 = ctypes.c_float
 _SIGS = {
     "echo_gate": (_I32, [_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _SZ, _P, _P]),
     "echo_gate_workspace_size": (_SZ, [_I32, _I32, _I32]),
+    "echo_gate_noalloc": (_I32, [_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P]),
     "echo_gate_sparse": (_I32, [_P, _P, _P, _I32, _I32, _I32, _P, _P, _I32, _P, _P, _P, _P, _P,
                                 _SZ, _P, _P]),
     "echo_gate_sparse_workspace_size": (_SZ, [_I32, _I32, _I32]),
@@ -169,6 +171,18 @@ def echo_gate(cand_offsets, parent, logq, R, N, budget, path_score, selected, nu
                             _stream(stream))
     if check:
         _check(code, "echo_gate")
+    return code
+
+
+def echo_gate_noalloc(cand_offsets, parent, logq, R, N, budget, path_score, selected,
+                      num_selected, status=None, stream=None, check=True):
+    """echo_gate with the library's fixed per-device workspace (no allocation;
+    overlapping calls on one device race)."""
+    code = load().echo_gate_noalloc(_ptr(cand_offsets), _ptr(parent), _ptr(logq), R, N, budget,
+                                    _ptr(path_score), _ptr(selected), _ptr(num_selected),
+                                    _ptr(status), _stream(stream))
+    if check:
+        _check(code, "echo_gate_noalloc")
     return code
 
 
