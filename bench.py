@@ -103,6 +103,103 @@ def traffic_from_profile(attn_src_hash, workload_key, path=PMC_SUMMARY):
     return d.get("hbm_bytes_per_launch")
 
 
+# MI355X shape used to normalise the counters: 8 XCDs of 32 CUs, 4 SIMDs per CU,
+# 4 shader engines per XCD, shader clock 2.4 GHz.
+N_XCD, N_SIMD, N_SE, CLOCK_HZ = 8, 1024, 32, 2.4e9
+
+
+def _pmc_medians(d, kernel="attn_main_kernel"):
+    """Median per dispatch of every counter of `kernel` in a rocprofv3 --pmc output dir."""
+    import csv
+    import glob
+    import statistics
+    vals = {}
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if kernel in r["Kernel_Name"]:
+                    vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    return {k: statistics.median(v) for k, v in vals.items()}, {k: len(v) for k, v in vals.items()}
+
+
+def pmc_summary(args):
+    """Counters of the attention kernel, normalised, written to <pmc_out>.json and .md.
+
+    Normalisation: GRBM_GUI_ACTIVE is summed over the 8 XCDs (cycles of one XCD =
+    GRBM_GUI_ACTIVE / 8); SQ_VALU_MFMA_BUSY_CYCLES sums the busy cycles of the matrix
+    units of all 1024 SIMDs (16 per v_mfma_f32_16x16x32_bf16), so the MFMA busy
+    fraction is SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 * 1024); SQ_BUSY_CYCLES
+    sums the 32 shader engines; SQ_WAVE_CYCLES and the SQ_WAIT_* counters count in the
+    same (quad-cycle) unit per wave, so their ratio is the fraction of a wave's life
+    spent waiting; instruction counts are per dispatch and divided by SQ_WAVES;
+    SQ_INSTS_VALU_MFMA_MOPS_BF16 counts 512-FLOP units; FETCH_SIZE and WRITE_SIZE (KiB)
+    are scaled by what they read for a plain device copy of known size."""
+    counters, samples = {}, {}
+    for d in args.pmc_summary:
+        m, n = _pmc_medians(d)
+        counters.update(m)
+        samples.update(n)
+    out = {"kernel": "attn_main_kernel",
+           "workload_key": {"config": args.config, "seed": args.seed, "gate_policy": args.gate_policy,
+                            "page_size": args.page_size, "serve": bool(args.serve)},
+           "attn_src_sha256": attn_source_hash(), "counters_median_per_dispatch": counters,
+           "dispatches_per_counter": samples, "commands": args.pmc_commands}
+    c = counters.get
+    der = {}
+    if c("GRBM_GUI_ACTIVE"):
+        cyc = c("GRBM_GUI_ACTIVE") / N_XCD
+        der["kernel_cycles_per_xcd"] = cyc
+        der["kernel_us_at_2400mhz"] = cyc / CLOCK_HZ * 1e6
+        if c("SQ_VALU_MFMA_BUSY_CYCLES") is not None:
+            der["mfma_busy_frac"] = c("SQ_VALU_MFMA_BUSY_CYCLES") / (cyc * N_SIMD)
+        if c("SQ_BUSY_CYCLES") is not None:
+            der["sq_busy_frac"] = c("SQ_BUSY_CYCLES") / (cyc * N_SE)
+        if c("SQ_INSTS_VALU_MFMA_MOPS_BF16") is not None:
+            fl = c("SQ_INSTS_VALU_MFMA_MOPS_BF16") * 512.0
+            der["mfma_flop_per_dispatch"] = fl
+            der["mfma_tflops"] = fl / (cyc / CLOCK_HZ) / 1e12
+    if c("SQ_WAVE_CYCLES"):
+        for k in ("SQ_WAIT_INST_ANY", "SQ_WAIT_ANY", "SQ_ACTIVE_INST_VALU"):
+            if c(k) is not None:
+                der[k.lower() + "_per_wave_cycle"] = c(k) / c("SQ_WAVE_CYCLES")
+    if c("SQ_WAVES"):
+        for k in ("SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_INSTS_SALU", "SQ_INSTS_LDS", "SQ_INSTS_VMEM",
+                  "SQ_INSTS_BRANCH", "SQ_INSTS_SMEM"):
+            if c(k) is not None:
+                der[k.lower() + "_per_wave"] = c(k) / c("SQ_WAVES")
+    if c("SQ_INSTS_LDS"):
+        if c("SQ_LDS_BANK_CONFLICT") is not None:
+            der["lds_bank_conflict_cycles_per_lds_inst"] = c("SQ_LDS_BANK_CONFLICT") / c("SQ_INSTS_LDS")
+    if args.pmc_copy and c("FETCH_SIZE") is not None and c("WRITE_SIZE") is not None:
+        cf, _ = _pmc_medians(args.pmc_copy[0], kernel="copyBuffer")
+        cw, _ = _pmc_medians(args.pmc_copy[1], kernel="copyBuffer")
+        fs = args.pmc_copy_bytes / 1024.0 / cf["FETCH_SIZE"]
+        ws = args.pmc_copy_bytes / 1024.0 / cw["WRITE_SIZE"]
+        der["copy_fetch_kib"] = cf["FETCH_SIZE"]
+        der["copy_write_kib"] = cw["WRITE_SIZE"]
+        der["fetch_scale"] = fs
+        der["write_scale"] = ws
+        out["hbm_bytes_per_launch"] = (c("FETCH_SIZE") * fs + c("WRITE_SIZE") * ws) * 1024.0
+    out["derived"] = der
+    with open(args.pmc_out + ".json", "w") as f:
+        json.dump(out, f, indent=1)
+    from synth.configs import DESCRIPTION
+    lines = [f"# rocprofv3 counters of attn_main_kernel, {DESCRIPTION.get(args.config, args.config)}, "
+             f"seed {args.seed}", "", "Passes (each its own run, from the repository root as $REPO):",
+             "", "```"] + list(args.pmc_commands) + ["```", "",
+             "| counter | median per dispatch |", "|---|---|"]
+    lines += [f"| {k} | {v:.0f} |" for k, v in sorted(counters.items())]
+    lines += ["", "| derived | value |", "|---|---|"]
+    lines += [f"| {k} | {v:.4g} |" for k, v in der.items()]
+    if "hbm_bytes_per_launch" in out:
+        lines += [f"| hbm_bytes_per_launch | {out['hbm_bytes_per_launch'] / 1e9:.4f} GB |"]
+    lines += ["", "Normalisation: " + " ".join(pmc_summary.__doc__.split("Normalisation: ")[1].split()),
+              "", f"sha256 of attn.hip + build.py at measurement: `{out['attn_src_sha256']}`", ""]
+    with open(args.pmc_out + ".md", "w") as f:
+        f.write("\n".join(lines))
+    log(f"wrote {args.pmc_out}.json and .md")
+
+
 def cpu_model():
     """The host CPU's model name (from /proc/cpuinfo) and the cores this process may use."""
     name = platform.processor() or "unknown"
@@ -277,6 +374,16 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES, five times (the "
                          "reference kernel that scales the HBM byte counters)")
+    ap.add_argument("--pmc-summary", nargs="+", metavar="DIR",
+                    help="only summarise rocprofv3 --pmc output directories of the attention "
+                         "kernel (the counter passes of --config/--seed, then the FETCH_SIZE and "
+                         "WRITE_SIZE passes of --copy-calibration) into --pmc-out .json/.md")
+    ap.add_argument("--pmc-copy", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="with --pmc-summary: the copy-calibration passes")
+    ap.add_argument("--pmc-copy-bytes", type=int, default=1 << 30)
+    ap.add_argument("--pmc-out", default=None, help="path prefix of the summary files")
+    ap.add_argument("--pmc-commands", nargs="*", default=[],
+                    help="the commands that produced the passes (recorded in the summary)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the verification "
@@ -284,6 +391,10 @@ def main():
         sys.exit(2)
 
     import numpy as np
+
+    if args.pmc_summary:
+        pmc_summary(args)
+        return
 
     if args.copy_calibration > 0:
         import torch

@@ -257,26 +257,23 @@ def test_head_layouts_every_row(hq, hkv):
     _check_all(b)
 
 
-@pytest.mark.parametrize("name,offset", [("tiny", 1), ("tiny", 3), ("l8b", 1), ("l8b", 2)])
-def test_mask_from_unaligned_selection(name, offset):
-    """The packed mask of a selection array that starts off a 16-byte boundary (the
-    byte-wise load path) and, for tiny, ends inside a 128-byte chunk: every output equal
-    to the oracle's."""
+def _check_mask_only(b, offset):
+    """echo_build_tree_mask on the oracle's selection stored `offset` bytes past a
+    16-byte boundary: every output equal to the oracle's."""
     import torch
     import paper_2604_09603_amd as pkg
-    b = synth.make_batch(name, 3)
     cfg = b["cfg"]
     g = oracle.gate(b["cand_offsets"], b["parent"], b["logq"], cfg.budget)
     m = oracle.build_tree_mask(b["cand_offsets"], b["parent"], b["token"], g["selected"],
                                b["root_token"], b["prefix_len"], cfg.budget, cfg.mask_words)
     R, N, B, W = cfg.R, int(b["cand_offsets"][-1]), cfg.budget, cfg.mask_words
-    print(f"[edges] unaligned selection {name} offset {offset} N={N}", flush=True)
     d = torch.device("cuda:0")
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(d)
     raw = torch.zeros(N + 64, dtype=torch.uint8, device=d)
-    sel = raw[offset:offset + N]
+    base = (-raw.data_ptr()) % 16
+    sel = raw[base + offset:base + offset + N]
     sel.copy_(dev(g["selected"].astype(np.uint8)))
-    assert sel.data_ptr() % 16 != 0
+    assert sel.data_ptr() % 16 == offset % 16
     cap = R + B
     i32 = lambda n: torch.full((n,), -7, dtype=torch.int32, device=d)
     q_offsets, slot_cand, slot_parent, slot_token, pos = i32(R + 1), i32(cap), i32(cap), i32(cap), i32(cap)
@@ -295,3 +292,28 @@ def test_mask_from_unaligned_selection(name, offset):
     tm = tree_mask.cpu().numpy().view(np.uint32).reshape(cap, W)
     assert np.array_equal(tm[:ns], np.asarray(m["tree_mask"]).reshape(-1, W)[:ns].view(np.uint32))
     assert int(status.cpu()[0]) == int(m["status"])
+
+
+@pytest.mark.parametrize("name,offset", [("tiny", 1), ("tiny", 3), ("l8b", 1), ("l8b", 2)])
+def test_mask_from_unaligned_selection(name, offset):
+    """The packed mask of a selection array that starts off a 16-byte boundary (the
+    byte-wise load path) and, for tiny, ends inside a 16-byte chunk."""
+    b = synth.make_batch(name, 3)
+    print(f"[edges] unaligned selection {name} offset {offset} N={int(b['cand_offsets'][-1])}",
+          flush=True)
+    _check_mask_only(b, offset)
+
+
+@pytest.mark.parametrize("offset", [0, 5])
+def test_mask_over_several_compaction_rounds(offset):
+    """More candidates than one round of the mask kernel's compaction reads
+    (1024 threads x 128 flags = 131072): 512 requests of 8 + 6 x 64 = 392 draft
+    nodes (N = 200704, two rounds, the second ending inside a wave's range),
+    budget 4096 spread over the whole pool; aligned and unaligned flags."""
+    cfg = synth.Config("rounds", 512, 7, 8, 3.0, 1000, 4096, 1, 1, 128, 0, 0, ("const", 0.5))
+    b = synth.make_batch(cfg, 11, attention=False)
+    b["prefix_len"] = np.random.default_rng(12).integers(0, 5000, 512).astype(np.int32)
+    N = int(b["cand_offsets"][-1])
+    assert N > 131072
+    print(f"[edges] multi-round compaction N={N} offset {offset}", flush=True)
+    _check_mask_only(b, offset)
