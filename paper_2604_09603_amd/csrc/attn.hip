@@ -52,7 +52,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 // 2^8 (in the exponent): probabilities stay <= 256, exact after normalisation.
 constexpr float kRescaleSlack = 8.0f;
 // A tile whose largest probability in a row exceeds this fraction of the
-// lane's running sum also multiplies V by the bf16 residual p - bf16(p) (see
+// row's running sum also multiplies V by the bf16 residual p - bf16(p) (see
 // compute_tile).
 constexpr float kSplitFrac = 1.0f / 16.0f;
 
@@ -724,13 +724,13 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
     // Where a few keys carry the row's weight, the rounding of their
     // probabilities moves the output by up to 2^-9 of the spread of their
     // values.  A key of this tile has at most 2^(mt - m) of weight; if that can
-    // exceed 1/16 of the lane's running sum (a lower bound of the row's final
-    // sum), the residuals p - bf16(p), rounded to bf16 too, go through a second
-    // product and into the normaliser, leaving 2^-17 of relative error on these
-    // weights.  Long rows over many keys take this path only on their first
-    // tiles and on outliers.
+    // exceed 1/16 of the row's running sum (the sum over its four lanes, a
+    // lower bound of the row's final sum), the residuals p - bf16(p), rounded
+    // to bf16 too, go through a second product and into the normaliser,
+    // leaving 2^-17 of relative error on these weights.  Long rows over many
+    // keys take this path only on their first tiles and on outliers.
     const float pmax = __builtin_amdgcn_exp2f(mt - rt[t].m);
-    if (__ballot(pmax > kSplitFrac * rt[t].l) != 0ull) {
+    if (__ballot(pmax > kSplitFrac * row_sum4(rt[t].l)) != 0ull) {
       uint4 pl;
       const auto res = [](float p, uint32_t hi2, int half) {
         const uint32_t b = half ? (hi2 & 0xFFFF0000u) : (hi2 << 16);
