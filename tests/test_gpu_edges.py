@@ -177,7 +177,8 @@ def test_maximum_batch_and_budget(budget):
     ro, rl, _ = oracle.tree_verify_attn(b["q"], b["k_new"], b["v_new"], b["k_cache"],
                                         b["v_cache"], b["kv_offsets"], m["q_offsets"],
                                         m["tree_mask"], cfg.hq, cfg.hkv, b["sm_scale"])
-    gc.compare_attn(res["out"], res["lse"], ro, rl, range(m["num_slots"]))
+    err = gc.compare_attn(res["out"], res["lse"], ro, rl, range(m["num_slots"]))
+    print(f"[edges] max sizes B={budget}: max abs {err[0]:.2e}, row rel {err[1]:.2e}", flush=True)
 
 
 @pytest.mark.parametrize("seed", range(4))
@@ -196,7 +197,8 @@ def test_few_key_rows_every_row(seed):
     ro, rl, _ = oracle.tree_verify_attn(b["q"], b["k_new"], b["v_new"], b["k_cache"],
                                         b["v_cache"], b["kv_offsets"], m["q_offsets"],
                                         m["tree_mask"], cfg.hq, cfg.hkv, b["sm_scale"])
-    gc.compare_attn(res["out"], res["lse"], ro, rl, range(m["num_slots"]))
+    err = gc.compare_attn(res["out"], res["lse"], ro, rl, range(m["num_slots"]))
+    print(f"[edges] few keys, seed {seed}: max abs {err[0]:.2e}, row rel {err[1]:.2e}", flush=True)
 
 
 @pytest.mark.parametrize("seed", range(2))

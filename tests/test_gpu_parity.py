@@ -90,14 +90,15 @@ def test_peaked_queries(name):
 def test_scaled_values(name):
     """Values (new and cached) scaled x4, plain and with queries also scaled x4
     (outputs of order four, weight on fewer keys): sampled rows of every preset,
-    every row for tiny, at the same absolute bounds."""
+    every row of tiny and of l8b (160 slots x 32 heads), at the same absolute
+    bounds."""
     for q_scale in (1.0, 4.0):
         b = synth.make_batch(name, 11, q_scale=q_scale, v_scale=4.0)
         ref = gc.oracle_front(b)
         st, res = gc.run_gpu(b, ref["target"])
         gc.compare_front(res, ref, int(b["cand_offsets"][-1]))
         m = ref["mask"]
-        rows = (list(range(m["num_slots"])) if name == "tiny" else
+        rows = (list(range(m["num_slots"])) if name in ("tiny", "l8b") else
                 gc.sample_rows(m["q_offsets"], np.random.default_rng(5)))
         ro, rl = _attn_ref(b, m, rows)
         err = gc.compare_attn(res["out"], res["lse"], ro, rl, rows)
