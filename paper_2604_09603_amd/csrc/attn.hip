@@ -87,9 +87,15 @@ struct AttnWs {
 
 __host__ __device__ inline size_t al(size_t x) { return (x + 255) / 256 * 256; }
 
-// Units never exceed one per request plus one per four streams.
+// Row passes of a request with fewer KV heads than a unit has waves: enough to
+// give every wave of its units a stream (see request_shape).
+__host__ __device__ inline int fill_passes(int hkv) { return (kWaves + hkv - 1) / hkv; }
+
+// Units never exceed one per request plus one per four streams; a request has at
+// most ceil(rows / 64) or fill_passes(hkv) passes per KV head.
 __host__ inline size_t unit_capacity(int R, int max_rows, int hq, int hkv) {
-  const size_t passes = size_t(R) + (size_t(max_rows) * (hq / hkv) + kPassRows - 1) / kPassRows;
+  const size_t passes = size_t(R) * size_t(fill_passes(hkv)) +
+                        (size_t(max_rows) * (hq / hkv) + kPassRows - 1) / kPassRows;
   return size_t(R) + (size_t(hkv) * passes + kWaves - 1) / kWaves;
 }
 
@@ -221,6 +227,10 @@ struct RequestShape {
 
 // A request's rows per head split into passes of at most 64 rows, as even as
 // possible; its hkv * passes streams form ceil(/4) groups over the same tiles.
+// With fewer KV heads than a unit has waves (one KV head, or a tensor-parallel
+// share of a few), that would leave waves idle: the rows are then split into
+// fill_passes(hkv) passes (at least one row each), whose streams read the same
+// head's tiles and share them in the caches.
 // `ok` is request_ok of request r (evaluated once per plan).  A paged request's
 // kb is its index (its block table row), a contiguous one's its first row.
 __device__ __forceinline__ RequestShape request_shape(const int32_t* q_offsets, const KvSource& kv,
@@ -239,6 +249,7 @@ __device__ __forceinline__ RequestShape request_shape(const int32_t* q_offsets, 
   const int rows = s.nsl * G;
   s.passes = (rows + kPassRows - 1) / kPassRows;
   if (s.passes == 0) return s;
+  s.passes = max(s.passes, min(rows, fill_passes(hkv)));
   s.rpp = (rows + s.passes - 1) / s.passes;
   s.ntail = (s.nsl + kTileKeys - 1) / kTileKeys;
   s.groups = (hkv * s.passes + kWaves - 1) / kWaves;

@@ -64,6 +64,10 @@ EXTRA_CONFIGS = {
     "g1_decode": Config("g1_decode", 64, 4, 4, 2.0, 32, 0, 8, 8, 128, 1024, 8192, ("const", 0.7)),
     "g1_tree": Config("g1_tree", 64, 4, 4, 2.0, 32, 128, 8, 8, 128, 1024, 8192, ("const", 0.7)),
     "g2_tree": Config("g2_tree", 64, 4, 4, 2.0, 32, 64, 16, 8, 128, 1024, 8192, ("const", 0.7)),
+    # the Qwen3-235B-shaped batch at the share one GPU holds under 4-way tensor
+    # parallelism over the KV heads: 16 query heads and one KV head
+    "q235b_tp4": Config("q235b_tp4", 128, 8, 10, 3.0, 151936, 256, 16, 1, 128, 1024, 8192,
+                        ("beta", 5.0, 4.0)),
 }
 CONFIGS.update(EXTRA_CONFIGS)
 
@@ -76,4 +80,5 @@ DESCRIPTION = {
     "g1_decode": "GQA group 1, decode only: batch 64, B=0, 8q/8kv, prefix 1024-8192",
     "g1_tree": "GQA group 1: batch 64, tree 4x4, B=128, 8q/8kv, prefix 1024-8192",
     "g2_tree": "GQA group 2: batch 64, tree 4x4, B=64, 16q/8kv, prefix 1024-8192",
+    "q235b_tp4": "Qwen3-235B-shaped layer at a TP-4 share: batch 128, tree 8x10, B=256, 16q/1kv, prefix 1024-8192",
 }

@@ -57,10 +57,12 @@ def test_presets_match_oracle(name, seed):
     _log(f"[parity] {name} seed={seed}: ok, attention max abs {err[0]:.2e}, row rel {err[1]:.2e}")
 
 
-@pytest.mark.parametrize("name", ["g1_decode", "g1_tree", "g2_tree"])
+@pytest.mark.parametrize("name", ["g1_decode", "g1_tree", "g2_tree", "q235b_tp4"])
 def test_narrow_groups_match_oracle(name):
     """GQA groups of one and two query heads (one row per stream in decode):
-    streams with fewer rows than one matrix tile, sampled rows against the oracle."""
+    streams with fewer rows than one matrix tile; and one KV head with a group of
+    16 (a TP-4 share of the Qwen3-235B-shaped batch): fewer streams per request than
+    a unit has waves.  Sampled rows against the oracle."""
     _log(f"[parity] {name}: generating")
     b = synth.make_batch(name, 2)
     ref = gc.oracle_front(b)
