@@ -584,6 +584,10 @@ struct RowTile {
   float m;       // softmax reference max of scaled logits (log2 units)
   float l;       // this lane's share of the running sum (for the LSE)
   float lq;      // the same over the bf16-rounded probabilities (normalises O)
+  float mgrow;   // m + kRescaleSlack: a tile max above it raises the reference
+  float negm;    // -m (0 while m is -inf): the exponent's offset
+  float thr;     // screen of the residual split: m + log2(row sum) - 5, taken
+                 // when last refreshed (see compute_tile)
 };
 
 // Per-lane LDS byte offsets of the swizzled fragment reads (lane constants; the
@@ -655,31 +659,42 @@ __device__ __forceinline__ void load_tile(const char* kt, const char* vt, const 
 
 // One 32-key tile (already in registers) against MT row tiles (all rows of the
 // unit).  masked: keys >= tn are invisible, and key j is visible to a row only
-// if bit j of its mask word is set.  The independent MFMA chains of the row
-// tiles and key subtiles are interleaved.
+// if bit j of its mask word is set.
+//
+// Row tile t's softmax runs between the S^T products of row tile t + 1 and the
+// P V products of row tile t - 1, which do not depend on it, one product at a
+// time between a few vector instructions: the matrix unit works on those
+// while the vector unit computes the probabilities.  (Left to itself the
+// scheduler issues the eight products of a group back to back, and a wave
+// issues in order, so nothing would overlap.)  Scheduling fences
+// (sched_barrier) hold that order; the arithmetic and its order per row are
+// the same as with the products grouped.
 template <int MT>
 __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*qf)[4],
                                              RowTile* rt, bool masked, int tn, float scale2,
                                              const uint32_t* mword) {
   const int lane = threadIdx.x & (kWave - 1);
   const int lg = lane >> 4;
-  // S^T = K Q^T: 2 subtiles x MT row tiles of independent accumulation chains
-  floatx4 st[MT][2];
+  floatx4 st[MT][2];  // S^T of each row tile: two 16-key subtiles
+  bf16x8 pf[MT];      // bf16 probabilities, the B operand of P V
+  // product j (0..7) of row tile t's S^T = K Q^T: key subtile j & 1, dims
+  // 32 (j >> 1) .. 32 (j >> 1) + 31
+  auto s_step = [&](int t, int j) {
+    const int s2 = j & 1, kk = j >> 1;
+    st[t][s2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+        f.kf[s2][kk], qf[t][kk], kk == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : st[t][s2], 0, 0, 0);
+  };
+  // product dt of row tile t's O^T += V^T P^T (dims 16 dt .. 16 dt + 15)
+  auto pv_step = [&](int t, int dt) {
+    rt[t].o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.vf[dt], pf[t], rt[t].o[dt], 0, 0, 0);
+  };
+#define ECHO_FENCE() __builtin_amdgcn_sched_barrier(0)
 #pragma unroll
-  for (int t = 0; t < MT; ++t)
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) st[t][s2] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2)
-#pragma unroll
-      for (int t = 0; t < MT; ++t)
-        st[t][s2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.kf[s2][kk], qf[t][kk], st[t][s2], 0, 0, 0);
-  // online softmax (base 2); lane holds keys 16*s2 + 4*lg + i of row lane%16
-  bf16x8 pf[MT];
+  for (int j = 0; j < 8; ++j) s_step(0, j);
 #pragma unroll
   for (int t = 0; t < MT; ++t) {
+    const bool nx = t + 1 < MT;
+    // lane holds keys 16*s2 + 4*lg + i of row lane%16
     float sv[8];
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2)
@@ -696,12 +711,47 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
           sv[4 * s2 + i] = ok ? sv[4 * s2 + i] : -__builtin_inff();
         }
     }
-    float mx = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
-                     fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
-    mx = row_max4(mx);
+    // row max (over the row's four lanes) beside row tile t + 1's S^T
+    ECHO_FENCE();
+    if (nx) s_step(t + 1, 0);
+    ECHO_FENCE();
+    const float a01 = fmaxf(sv[0], sv[1]), a23 = fmaxf(sv[2], sv[3]);
+    ECHO_FENCE();
+    if (nx) s_step(t + 1, 1);
+    ECHO_FENCE();
+    const float a47 = fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7]));
+    ECHO_FENCE();
+    if (nx) s_step(t + 1, 2);
+    ECHO_FENCE();
+    float mx = fmaxf(fmaxf(a01, a23), a47);
+    ECHO_FENCE();
+    if (nx) s_step(t + 1, 3);
+    ECHO_FENCE();
+    {
+      const uint32_t u = __float_as_uint(mx);
+      const auto x = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+      mx = fmaxf(__uint_as_float(x[0]), __uint_as_float(x[1]));
+    }
+    ECHO_FENCE();
+    if (nx) s_step(t + 1, 4);
+    ECHO_FENCE();
+    {
+      const uint32_t u = __float_as_uint(mx);
+      const auto x = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+      mx = fmaxf(__uint_as_float(x[0]), __uint_as_float(x[1]));
+    }
+    ECHO_FENCE();
+    if (nx) s_step(t + 1, 5);
+    ECHO_FENCE();
     const float mt = mx * scale2;  // -inf stays -inf
     // raise the reference only when a logit would exceed it by more than the slack
-    const bool grow = mt > rt[t].m + kRescaleSlack;
+    const bool grow = mt > rt[t].mgrow;
+    ECHO_FENCE();
+    if (nx) {
+      s_step(t + 1, 6);
+      s_step(t + 1, 7);
+    }
+    ECHO_FENCE();
     if (__ballot(grow) != 0ull) {
       const float alpha = grow ? __builtin_amdgcn_exp2f(rt[t].m - mt) : 1.0f;  // 0 from -inf
       rt[t].l *= alpha;
@@ -709,14 +759,21 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) rt[t].o[dt] *= alpha;
       rt[t].m = grow ? mt : rt[t].m;
+      rt[t].mgrow = rt[t].m + kRescaleSlack;
+      rt[t].negm = rt[t].m == -__builtin_inff() ? 0.0f : -rt[t].m;
     }
-    const float neg_m = rt[t].m == -__builtin_inff() ? 0.0f : -rt[t].m;
+    // probabilities beside row tile t - 1's P V
+    const float neg_m = rt[t].negm;
     float psum = 0.0f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
+      ECHO_FENCE();
+      if (t >= 1) pv_step(t - 1, e);
+      ECHO_FENCE();
       sv[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[e], scale2, neg_m));
       psum += sv[e];
     }
+    ECHO_FENCE();
     rt[t].l += psum;
     uint4 pk;
     pk.x = pack_bf16x2(sv[0], sv[1]);
@@ -740,8 +797,20 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
     // to bf16 too, go through a second product and into the normaliser,
     // leaving 2^-17 of relative error on these weights.  Long rows over many
     // keys take this path only on their first tiles and on outliers.
-    const float pmax = __builtin_amdgcn_exp2f(mt - rt[t].m);
-    if (__ballot(pmax > kSplitFrac * row_sum4(rt[t].l)) != 0ull) {
+    //
+    // The test is screened first: m + log2(row sum) is the log2 of the row's
+    // running sum in absolute units, which only grows from tile to tile (a
+    // rescale moves m and the sum together), so thr = m + log2(sum) - 5 taken
+    // at any earlier tile is at most the test's threshold now, m + log2(sum)
+    // - 4, and a tile max at or below it cannot pass the test.  The exact test
+    // (and a refresh of thr) runs only when the screen lets a tile through.
+    bool split = false;
+    if (__ballot(mt > rt[t].thr) != 0ull) {
+      const float rs = row_sum4(rt[t].l);
+      split = __ballot(__builtin_amdgcn_exp2f(mt - rt[t].m) > kSplitFrac * rs) != 0ull;
+      rt[t].thr = rt[t].m + __builtin_amdgcn_logf(rs) - 5.0f;
+    }
+    if (split) {
       uint4 pl;
       const auto res = [](float p, uint32_t hi2, int half) {
         const uint32_t b = half ? (hi2 & 0xFFFF0000u) : (hi2 << 16);
@@ -758,12 +827,9 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
         rt[t].o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.vf[dt], plo, rt[t].o[dt], 0, 0, 0);
     }
   }
-  // O^T += V^T P^T
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt)
-#pragma unroll
-    for (int t = 0; t < MT; ++t)
-      rt[t].o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.vf[dt], pf[t], rt[t].o[dt], 0, 0, 0);
+  for (int dt = 0; dt < 8; ++dt) pv_step(MT - 1, dt);
+#undef ECHO_FENCE
 }
 
 // The wave's index in the workgroup, known to the compiler as wave-uniform (so
@@ -951,6 +1017,9 @@ __device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws,
     rt[i].m = -__builtin_inff();
     rt[i].l = 0.0f;
     rt[i].lq = 0.0f;
+    rt[i].mgrow = -__builtin_inff();
+    rt[i].negm = 0.0f;
+    rt[i].thr = -__builtin_inff();
   }
   wait_vm<0>();
 

@@ -221,6 +221,60 @@ def test_few_key_rows_scaled_values_every_row(seed):
           flush=True)
 
 
+@pytest.mark.parametrize("seed", range(2))
+def test_late_dominant_key_every_row(seed):
+    """A key in the last two tiles of a long prefix carries about 40% of every
+    row's weight, and a key in the first prefix tile, one unit of log2 below
+    it, about 20% (each request's queries are one vector per KV head; both keys
+    are that vector scaled to the wanted logit; the other keys and the tree's
+    keys have logits of order 0.25).  The early key raises the softmax
+    reference, so the late key's probability is 2^(1 + e), not a power of two,
+    and its bf16 rounding moves the output by up to 2^-9 of the value spread
+    (6e-3 to 9e-3 on these batches) unless the residual product runs (3e-4).
+    The kernel screens that test with a threshold taken at earlier tiles; the
+    bound of 1.5e-3 on every row shows the late tile still got through."""
+    rng = np.random.default_rng(500 + seed)
+    R, hq, hkv = 8, 32, 2
+    G = hq // hkv
+    pool = synth.micro_pool(rng, R, 9, p_neg_inf=0.0)
+    b = make_micro_batch(pool, 24, hq=hq, hkv=hkv, p_range=(1800, 2600), seed=seed,
+                         v_scale=4.0)
+    scale = float(b["sm_scale"])
+    kf = synth.bf16_bits_to_f32(b["k_cache"]) * np.float32(0.25)
+    kn = synth.bf16_bits_to_f32(b["k_new"]) * np.float32(0.25)
+    q = synth.bf16_bits_to_f32(b["q"])
+    P, kvo = b["prefix_len"], b["kv_offsets"]
+    qo = _front_ref(b)["mask"]["q_offsets"]   # the slots do not depend on q or k
+    for r in range(R):
+        early = int(kvo[r]) + int(rng.integers(0, 32))
+        late = int(kvo[r]) + int(P[r]) - 1 - int(rng.integers(0, 64))
+        for h in range(hkv):
+            q0 = synth.bf16_bits_to_f32(
+                synth.f32_to_bf16_bits(rng.standard_normal(128).astype(np.float32)))
+            q[qo[r]:qo[r + 1], h * G:(h + 1) * G, :] = q0
+            unit = q0 / np.float32(float(q0 @ q0) * scale)   # logit 1 (natural units)
+            logit = math.log(float(P[r]))
+            kf[late, h, :] = unit * np.float32(logit)
+            kf[early, h, :] = unit * np.float32(logit - math.log(2.0))
+    b["q"] = synth.f32_to_bf16_bits(q)
+    b["k_cache"] = synth.f32_to_bf16_bits(kf)
+    b["k_new"] = synth.f32_to_bf16_bits(kn)
+    ref = _front_ref(b)
+    st, res = gc.run_gpu(b, ref["target"])
+    gc.compare_front(res, ref, int(b["cand_offsets"][-1]))
+    cfg = b["cfg"]
+    m = ref["mask"]
+    ro, rl, _ = oracle.tree_verify_attn(b["q"], b["k_new"], b["v_new"], b["k_cache"],
+                                        b["v_cache"], b["kv_offsets"], m["q_offsets"],
+                                        m["tree_mask"], cfg.hq, cfg.hkv, b["sm_scale"])
+    nq = m["num_slots"]
+    gc.compare_attn(res["out"], res["lse"], ro, rl, range(nq))
+    err = np.abs(res["out"][:nq].astype(np.float64) - ro[:nq]).max()
+    print(f"[edges] late dominant key, seed {seed}: max abs {err:.2e} over {nq * hq} rows",
+          flush=True)
+    assert err <= 1.5e-3, f"max abs error {err:.3e}: the late tile's residual product did not run"
+
+
 def test_empty_requests_and_prefixes():
     offs = np.array([0, 0, 4, 4, 7], np.int32)            # requests 0 and 2 have no candidates
     parent = np.array([-1, 0, 0, 1, -1, -1, 1], np.int32)
