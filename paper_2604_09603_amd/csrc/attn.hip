@@ -671,7 +671,7 @@ __device__ __forceinline__ void load_tile(const char* kt, const char* vt, const 
 // the same as with the products grouped.
 template <int MT>
 __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*qf)[4],
-                                             RowTile* rt, bool masked, int tn, float scale2,
+                                             RowTile* rt, bool masked, float scale2,
                                              const uint32_t* mword) {
   const int lane = threadIdx.x & (kWave - 1);
   const int lg = lane >> 4;
@@ -707,11 +707,15 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int key = 16 * s2 + 4 * lg + i;
-          const bool ok = key < tn && ((mword[t] >> key) & 1u);
+          const bool ok = (mword[t] >> key) & 1u;
           sv[4 * s2 + i] = ok ? sv[4 * s2 + i] : -__builtin_inff();
         }
     }
-    // row max (over the row's four lanes) beside row tile t + 1's S^T
+    // this lane's max over its 8 of the row's 32 keys, beside row tile t + 1's
+    // S^T.  A lane's max exceeds a bound in some lane of a row
+    // exactly when the row's max does, so the rescale test and the residual
+    // screen need no reduction over the row's four lanes; the rare branches
+    // that do take the row's max.
     ECHO_FENCE();
     if (nx) s_step(t + 1, 0);
     ECHO_FENCE();
@@ -723,36 +727,11 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
     ECHO_FENCE();
     if (nx) s_step(t + 1, 2);
     ECHO_FENCE();
-    float mx = fmaxf(fmaxf(a01, a23), a47);
-    ECHO_FENCE();
-    if (nx) s_step(t + 1, 3);
-    ECHO_FENCE();
-    {
-      const uint32_t u = __float_as_uint(mx);
-      const auto x = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-      mx = fmaxf(__uint_as_float(x[0]), __uint_as_float(x[1]));
-    }
-    ECHO_FENCE();
-    if (nx) s_step(t + 1, 4);
-    ECHO_FENCE();
-    {
-      const uint32_t u = __float_as_uint(mx);
-      const auto x = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-      mx = fmaxf(__uint_as_float(x[0]), __uint_as_float(x[1]));
-    }
-    ECHO_FENCE();
-    if (nx) s_step(t + 1, 5);
-    ECHO_FENCE();
-    const float mt = mx * scale2;  // -inf stays -inf
+    const float lmt = fmaxf(fmaxf(a01, a23), a47) * scale2;  // -inf stays -inf
     // raise the reference only when a logit would exceed it by more than the slack
-    const bool grow = mt > rt[t].mgrow;
-    ECHO_FENCE();
-    if (nx) {
-      s_step(t + 1, 6);
-      s_step(t + 1, 7);
-    }
-    ECHO_FENCE();
-    if (__ballot(grow) != 0ull) {
+    if (__ballot(lmt > rt[t].mgrow) != 0ull) {
+      const float mt = row_max4(lmt);
+      const bool grow = mt > rt[t].mgrow;
       const float alpha = grow ? __builtin_amdgcn_exp2f(rt[t].m - mt) : 1.0f;  // 0 from -inf
       rt[t].l *= alpha;
       rt[t].lq *= alpha;
@@ -762,13 +741,15 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
       rt[t].mgrow = rt[t].m + kRescaleSlack;
       rt[t].negm = rt[t].m == -__builtin_inff() ? 0.0f : -rt[t].m;
     }
-    // probabilities beside row tile t - 1's P V
+    // probabilities beside row tile t - 1's P V and the rest of row tile t + 1's S^T
     const float neg_m = rt[t].negm;
     float psum = 0.0f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       ECHO_FENCE();
       if (t >= 1) pv_step(t - 1, e);
+      ECHO_FENCE();
+      if (nx && e < 5) s_step(t + 1, 3 + e);
       ECHO_FENCE();
       sv[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[e], scale2, neg_m));
       psum += sv[e];
@@ -805,7 +786,8 @@ __device__ __forceinline__ void compute_tile(const TileFrags& f, const bf16x8 (*
     // - 4, and a tile max at or below it cannot pass the test.  The exact test
     // (and a refresh of thr) runs only when the screen lets a tile through.
     bool split = false;
-    if (__ballot(mt > rt[t].thr) != 0ull) {
+    if (__ballot(lmt > rt[t].thr) != 0ull) {
+      const float mt = row_max4(lmt);
       const float rs = row_sum4(rt[t].l);
       split = __ballot(__builtin_amdgcn_exp2f(mt - rt[t].m) > kSplitFrac * rs) != 0ull;
       rt[t].thr = rt[t].m + __builtin_amdgcn_logf(rs) - 5.0f;
@@ -1054,13 +1036,17 @@ __device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws,
 #pragma unroll
       for (int i = 0; i < MT; ++i) word[i] = 0xFFFFFFFFu;
     }
+    // keys >= tn are invisible too: one limit per tile, in the words
+    const uint32_t lim = tn >= kTileKeys ? 0xFFFFFFFFu : ((1u << tn) - 1u);
+#pragma unroll
+    for (int i = 0; i < MT; ++i) word[i] &= lim;
     // tile -> registers, then refill the stage at once: the ring stays full
     // while the tile is multiplied
     TileFrags f;
     load_tile(stg, stg + kTileBytes, lof, f);
     wait_lds();
     issue_next(is, a, ws, nunits, lo, hi, wid, ring_lds, cp);
-    compute_tile<MT>(f, qf, rt, masked, tn, a.scale2, word);
+    compute_tile<MT>(f, qf, rt, masked, a.scale2, word);
   }
 
   // ---- output of the segment ----
