@@ -24,7 +24,8 @@
 //                 barrier is needed: every wave owns its ring and its softmax
 //                 state.  S^T = K Q^T and O^T = V^T P^T on
 //                 v_mfma_f32_16x16x32_bf16 (fp32 accumulation), online softmax
-//                 in base 2, ancestor bitmask on tree-tail tiles.  A unit that
+//                 in base 2 between the products of the neighbouring 16-row
+//                 tiles, ancestor bitmask on tree-tail tiles.  A unit that
 //                 lies inside one range is normalised and written to out/lse; a
 //                 cut unit leaves one partial (O, max, sums) per stream and
 //                 workgroup.
