@@ -76,10 +76,13 @@ def attn_algorithmic(batch, res, cfg):
 
 
 def attn_source_hash():
-    """sha256 of what the attention kernel is built from: its source and the build
-    script (which holds its compiler flags)."""
+    """sha256 of what the attention kernel is built from: its source, the header with
+    its workspace layout and plan, and the build script (which holds its compiler
+    flags)."""
     h = hashlib.sha256()
-    for rel in (("paper_2604_09603_amd", "csrc", "attn.hip"), ("paper_2604_09603_amd", "build.py")):
+    for rel in (("paper_2604_09603_amd", "csrc", "attn.hip"),
+                ("paper_2604_09603_amd", "csrc", "attn_device.h"),
+                ("paper_2604_09603_amd", "build.py")):
         with open(os.path.join(ROOT, *rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
@@ -194,7 +197,7 @@ def pmc_summary(args):
     if "hbm_bytes_per_launch" in out:
         lines += [f"| hbm_bytes_per_launch | {out['hbm_bytes_per_launch'] / 1e9:.4f} GB |"]
     lines += ["", "Normalisation: " + " ".join(pmc_summary.__doc__.split("Normalisation: ")[1].split()),
-              "", f"sha256 of attn.hip + build.py at measurement: `{out['attn_src_sha256']}`", ""]
+              "", f"sha256 of attn.hip + attn_device.h + build.py at measurement: `{out['attn_src_sha256']}`", ""]
     with open(args.pmc_out + ".md", "w") as f:
         f.write("\n".join(lines))
     log(f"wrote {args.pmc_out}.json and .md")
@@ -369,6 +372,9 @@ def main():
                     help="the serving step: paged cache (64-row pages unless --page-size), "
                          "acceptance from bf16 target logits (echo_accept_logits) and the KV "
                          "commit of the accepted path (echo_commit_kv)")
+    ap.add_argument("--separate-calls", action="store_true",
+                    help="time the step as the four calls (gate, mask, attention, accept) "
+                         "instead of the one echo_verify_step call")
     ap.add_argument("--graph", action="store_true",
                     help="capture one step in a HIP graph and time graph replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -468,22 +474,25 @@ def main():
         flush_rows = half.shape[1] // (4 * 256)
     torch.cuda.synchronize()
 
+    # the step: one echo_verify_step call where it covers the configuration (top-B
+    # gate, contiguous cache, acceptance from target tokens), else the four calls
+    run_step = st.run_fused if st.fused_ok() and not args.separate_calls else st.run
     log(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):
-        st.run()
+        run_step()
     torch.cuda.synchronize()
-    step_fn = st.run
+    step_fn = run_step
     graph = None
     if args.graph:
         graph = torch.cuda.CUDAGraph()
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(side):
-            st.run()                      # a warm launch on the capture stream
+            run_step()                    # a warm launch on the capture stream
         torch.cuda.current_stream().wait_stream(side)
         torch.cuda.synchronize()
         with torch.cuda.graph(graph):
-            st.run()
+            run_step()
         torch.cuda.synchronize()
         step_fn = graph.replay
         for _ in range(3):
@@ -645,6 +654,7 @@ def main():
             "checkpoints": checkpoints, "elastic_widths": elastic,
             "kv_layout": f"paged, {page_size}-row pages" if page_size else "contiguous",
             "serve_step": bool(args.serve), "hip_graph": bool(args.graph),
+            "entry_point": "echo_verify_step" if run_step == st.run_fused else "four calls",
         },
         "timing": {
             "protocol": (f"value and ms_per_step: median of the {args.steps} timed steps, one "

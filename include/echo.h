@@ -312,6 +312,33 @@ int32_t echo_accept(const int32_t* q_offsets, const int32_t* slot_parent,
                     echo_stream_t stream);
 
 /*
+ * echo_verify_step -- the four calls above in one: echo_gate,
+ * echo_build_tree_mask, echo_tree_verify_attn (contiguous cache) and
+ * echo_accept on one stream, with the same arguments (in that order; the
+ * mask's unused workspace is dropped, `token` is the mask's candidate tokens,
+ * `max_rows` serves the attention and the acceptance) and bit-identical
+ * outputs and status bits.  It runs the gate's last phase, flatten & pack and
+ * the attention's plan in one single-workgroup launch: the three are one
+ * workgroup each and run back to back, and as separate launches each spends
+ * 3-4 us starting before its first data arrives.  Every check of the four
+ * calls runs before anything is launched; a failing check launches nothing.
+ * Needs mask_words * 32 >= budget + 1 and the same LDS bound as the mask
+ * call (ECHO_ERR_UNSUPPORTED beyond it).
+ */
+int32_t echo_verify_step(
+    const int32_t* cand_offsets, const int32_t* parent, const float* logq, const int32_t* token,
+    int32_t R, int32_t N, int32_t budget, float* path_score, uint8_t* selected,
+    int32_t* num_selected, void* gate_workspace, size_t gate_workspace_bytes,
+    const int32_t* root_token, const int32_t* prefix_len, int32_t* q_offsets, int32_t* slot_cand,
+    int32_t* slot_parent, int32_t* slot_token, int32_t* position_ids, uint32_t* tree_mask,
+    int32_t mask_words, const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
+    const uint16_t* k_cache, const uint16_t* v_cache, const int64_t* kv_offsets, int64_t kv_rows,
+    int32_t max_rows, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+    float sm_scale, float* out, float* lse, void* attn_workspace, size_t attn_workspace_bytes,
+    const int32_t* target_token, int32_t max_depth, int32_t* accept_len, int32_t* accept_slots,
+    int32_t* bonus_token, int32_t* status, echo_stream_t stream);
+
+/*
  * echo_accept_logits -- echo_accept with the target tokens taken from the
  * target model's logits: the greedy (temperature 0) token after slot s is the
  * argmax of logits[s][0 .. vocab), compared as floats (-0 == +0), NaN never

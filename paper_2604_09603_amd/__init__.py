@@ -38,7 +38,8 @@ EXPORTS = [
     "echo_tree_verify_attn", "echo_tree_verify_attn_workspace_size",
     "echo_tree_verify_attn_paged", "echo_accept_logits", "echo_commit_kv",
     "echo_accept", "echo_tree_verify_attn_timed", "echo_tree_verify_attn_paged_timed",
-    "echo_probe_stream_read", "echo_gate_noalloc", "echo_status_string", "echo_version",
+    "echo_probe_stream_read", "echo_gate_noalloc", "echo_verify_step", "echo_status_string",
+    "echo_version",
 ]
 GATE_SCRATCH_BYTES = 8 << 20
 
@@ -81,6 +82,11 @@ _SIGS = {
                                                  _P, _I32, _I32, _I32, _I32, _I32, _I32, _F32, _P,
                                                  _P, _P, _SZ, _P, _P, _P, _P]),
     "echo_probe_stream_read": (_I32, [_P, _P, _I64, _I32, _I32, _P, _P]),
+    "echo_verify_step": (_I32, [_P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _SZ,
+                                _P, _P, _P, _P, _P, _P, _P, _P, _I32,
+                                _P, _P, _P, _P, _P, _P, _I64, _I32, _I32, _I32, _I32, _F32, _P,
+                                _P, _P, _SZ,
+                                _P, _I32, _P, _P, _P, _P, _P]),
     "echo_status_string": (ctypes.c_char_p, [_I32]),
     "echo_version": (ctypes.c_char_p, []),
 }
@@ -289,6 +295,29 @@ def echo_accept(q_offsets, slot_parent, slot_token, target_token, R, max_rows, m
                               _stream(stream))
     if check:
         _check(code, "echo_accept")
+    return code
+
+
+def echo_verify_step(cand_offsets, parent, logq, token, R, N, budget, path_score, selected,
+                     num_selected, gate_workspace, root_token, prefix_len, q_offsets, slot_cand,
+                     slot_parent, slot_token, position_ids, tree_mask, mask_words, q, k_new, v_new,
+                     k_cache, v_cache, kv_offsets, kv_rows, max_rows, hq, hkv, head_dim, sm_scale,
+                     out, lse, attn_workspace, target_token, max_depth, accept_len, accept_slots,
+                     bonus_token, status=None, stream=None, check=True):
+    """The four stages of a step in one call (gate, flatten & pack, attention over a
+    contiguous cache, acceptance); the arguments of the four calls in order."""
+    code = load().echo_verify_step(
+        _ptr(cand_offsets), _ptr(parent), _ptr(logq), _ptr(token), R, N, budget, _ptr(path_score),
+        _ptr(selected), _ptr(num_selected), _ptr(gate_workspace),
+        gate_workspace.numel() * gate_workspace.element_size(), _ptr(root_token),
+        _ptr(prefix_len), _ptr(q_offsets), _ptr(slot_cand), _ptr(slot_parent), _ptr(slot_token),
+        _ptr(position_ids), _ptr(tree_mask), mask_words, _ptr(q), _ptr(k_new), _ptr(v_new),
+        _ptr(k_cache), _ptr(v_cache), _ptr(kv_offsets), int(kv_rows), max_rows, hq, hkv, head_dim,
+        float(sm_scale), _ptr(out), _ptr(lse), _ptr(attn_workspace),
+        attn_workspace.numel() * attn_workspace.element_size(), _ptr(target_token), max_depth,
+        _ptr(accept_len), _ptr(accept_slots), _ptr(bonus_token), _ptr(status), _stream(stream))
+    if check:
+        _check(code, "echo_verify_step")
     return code
 
 

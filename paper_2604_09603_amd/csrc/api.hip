@@ -35,14 +35,16 @@ inline hipStream_t as_stream(echo_stream_t s) { return reinterpret_cast<hipStrea
 // scales it afterwards, which is only valid for a positive finite scale.
 inline bool scale_ok(float s) { return s > 0.0f && s <= 3.4028234663852886e38f; }
 
-// Host-side checks and argument packing of the contiguous-cache attention.
-int32_t attn_contiguous(const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
-                        const uint16_t* k_cache, const uint16_t* v_cache, const int64_t* kv_offsets,
-                        int64_t kv_rows, const int32_t* q_offsets, const uint32_t* tree_mask,
-                        int32_t mask_words, int32_t R, int32_t max_rows, int32_t num_q_heads,
-                        int32_t num_kv_heads, int32_t head_dim, float sm_scale, float* out,
-                        float* lse, void* workspace, size_t workspace_bytes, int32_t* status,
-                        hipEvent_t ev_start, hipEvent_t ev_stop, hipStream_t stream) {
+// Host-side checks and argument packing of the contiguous-cache attention:
+// ECHO_OK with *a filled, or the error code.
+int32_t attn_contiguous_args(const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
+                             const uint16_t* k_cache, const uint16_t* v_cache,
+                             const int64_t* kv_offsets, int64_t kv_rows, const int32_t* q_offsets,
+                             const uint32_t* tree_mask, int32_t mask_words, int32_t R,
+                             int32_t max_rows, int32_t num_q_heads, int32_t num_kv_heads,
+                             int32_t head_dim, float sm_scale, float* out, float* lse,
+                             void* workspace, size_t workspace_bytes, int32_t* status,
+                             hipEvent_t ev_start, hipEvent_t ev_stop, echo::AttnArgs* a_out) {
   if (R < 1 || max_rows < 0 || num_q_heads < 1 || num_kv_heads < 1 || mask_words < 1 ||
       kv_rows < 0)
     return ECHO_ERR_INVALID_ARG;
@@ -62,8 +64,8 @@ int32_t attn_contiguous(const uint16_t* q, const uint16_t* k_new, const uint16_t
                         reinterpret_cast<uintptr_t>(v_new) | reinterpret_cast<uintptr_t>(k_cache) |
                         reinterpret_cast<uintptr_t>(v_cache) | reinterpret_cast<uintptr_t>(out);
   if (mis & 15u) return ECHO_ERR_INVALID_ARG;
-  if (max_rows == 0) return ECHO_OK;
-  echo::AttnArgs a{};
+  echo::AttnArgs& a = *a_out;
+  a = echo::AttnArgs{};
   a.q = q;
   a.k_new = k_new;
   a.v_new = v_new;
@@ -85,6 +87,23 @@ int32_t attn_contiguous(const uint16_t* q, const uint16_t* k_new, const uint16_t
   a.status = status;
   a.ev_start = ev_start;
   a.ev_stop = ev_stop;
+  return ECHO_OK;
+}
+
+int32_t attn_contiguous(const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
+                        const uint16_t* k_cache, const uint16_t* v_cache, const int64_t* kv_offsets,
+                        int64_t kv_rows, const int32_t* q_offsets, const uint32_t* tree_mask,
+                        int32_t mask_words, int32_t R, int32_t max_rows, int32_t num_q_heads,
+                        int32_t num_kv_heads, int32_t head_dim, float sm_scale, float* out,
+                        float* lse, void* workspace, size_t workspace_bytes, int32_t* status,
+                        hipEvent_t ev_start, hipEvent_t ev_stop, hipStream_t stream) {
+  echo::AttnArgs a;
+  const int32_t rc = attn_contiguous_args(q, k_new, v_new, k_cache, v_cache, kv_offsets, kv_rows,
+                                          q_offsets, tree_mask, mask_words, R, max_rows,
+                                          num_q_heads, num_kv_heads, head_dim, sm_scale, out, lse,
+                                          workspace, workspace_bytes, status, ev_start, ev_stop,
+                                          &a);
+  if (rc != ECHO_OK || max_rows == 0) return rc;
   return echo::launch_tree_verify_attn(a, stream);
 }
 
@@ -337,6 +356,80 @@ int32_t echo_accept(const int32_t* q_offsets, const int32_t* slot_parent,
   return echo::launch_accept(q_offsets, slot_parent, slot_token, target_token, R, max_rows,
                              max_depth, accept_len, accept_slots, bonus_token, status,
                              as_stream(stream));
+}
+
+int32_t echo_verify_step(
+    const int32_t* cand_offsets, const int32_t* parent, const float* logq, const int32_t* token,
+    int32_t R, int32_t N, int32_t budget, float* path_score, uint8_t* selected,
+    int32_t* num_selected, void* gate_workspace, size_t gate_workspace_bytes,
+    const int32_t* root_token, const int32_t* prefix_len, int32_t* q_offsets, int32_t* slot_cand,
+    int32_t* slot_parent, int32_t* slot_token, int32_t* position_ids, uint32_t* tree_mask,
+    int32_t mask_words, const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
+    const uint16_t* k_cache, const uint16_t* v_cache, const int64_t* kv_offsets, int64_t kv_rows,
+    int32_t max_rows, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+    float sm_scale, float* out, float* lse, void* attn_workspace, size_t attn_workspace_bytes,
+    const int32_t* target_token, int32_t max_depth, int32_t* accept_len, int32_t* accept_slots,
+    int32_t* bonus_token, int32_t* status, echo_stream_t stream) {
+  // every check of the four calls, before anything is launched
+  if (R < 1 || N < 0 || budget < 0) return ECHO_ERR_INVALID_ARG;
+  if (R > ECHO_MAX_REQUESTS || budget > ECHO_MAX_BUDGET) return ECHO_ERR_UNSUPPORTED;
+  if (!cand_offsets || !num_selected || !gate_workspace) return ECHO_ERR_INVALID_ARG;
+  if (N > 0 && (!parent || !logq || !selected || !token)) return ECHO_ERR_INVALID_ARG;
+  if (!aligned256(gate_workspace) ||
+      gate_workspace_bytes < echo::gate_workspace_bytes(R, N, budget))
+    return ECHO_ERR_WORKSPACE;
+  if (int64_t(mask_words) * 32 < int64_t(budget) + 1) return ECHO_ERR_INVALID_ARG;
+  if (!root_token || !prefix_len || !q_offsets || !slot_cand || !slot_parent || !slot_token ||
+      !position_ids || !tree_mask)
+    return ECHO_ERR_INVALID_ARG;
+  if (echo::mask_lds_bytes(R, budget) > 150 * 1024) return ECHO_ERR_UNSUPPORTED;
+  echo::AttnArgs a;
+  int32_t rc = attn_contiguous_args(q, k_new, v_new, k_cache, v_cache, kv_offsets, kv_rows,
+                                    q_offsets, tree_mask, mask_words, R, max_rows, num_q_heads,
+                                    num_kv_heads, head_dim, sm_scale, out, lse, attn_workspace,
+                                    attn_workspace_bytes, status, nullptr, nullptr, &a);
+  if (rc != ECHO_OK) return rc;
+  if (max_depth < 1) return ECHO_ERR_INVALID_ARG;
+  if (max_depth > ECHO_MAX_DEPTH) return ECHO_ERR_UNSUPPORTED;
+  if (!accept_len || !accept_slots || !bonus_token) return ECHO_ERR_INVALID_ARG;
+  if (max_rows > 0 && !target_token) return ECHO_ERR_INVALID_ARG;
+  hipStream_t s = as_stream(stream);
+  rc = echo::launch_gate_select_only(cand_offsets, parent, logq, R, N, budget, path_score,
+                                     selected, num_selected, gate_workspace, status, s);
+  if (rc != ECHO_OK) return rc;
+  echo::FrontLaunch f;
+  f.N = N;
+  f.R = R;
+  f.budget = budget;
+  f.mask_words = mask_words;
+  f.gate_workspace = gate_workspace;
+  f.selected = selected;
+  f.cand_offsets = cand_offsets;
+  f.parent = parent;
+  f.token = token;
+  f.root_token = root_token;
+  f.prefix_len = prefix_len;
+  f.q_offsets = q_offsets;
+  f.slot_cand = slot_cand;
+  f.slot_parent = slot_parent;
+  f.slot_token = slot_token;
+  f.position_ids = position_ids;
+  f.tree_mask = tree_mask;
+  f.kv_offsets = kv_offsets;
+  f.kv_rows = kv_rows;
+  f.max_rows = max_rows;
+  f.hq = num_q_heads;
+  f.hkv = num_kv_heads;
+  f.attn_workspace = attn_workspace;
+  f.status = status;
+  rc = echo::launch_front(f, s);
+  if (rc != ECHO_OK) return rc;
+  if (max_rows > 0) {
+    rc = echo::launch_tree_verify_attn_planned(a, s);
+    if (rc != ECHO_OK) return rc;
+  }
+  return echo::launch_accept(q_offsets, slot_parent, slot_token, target_token, R, max_rows,
+                             max_depth, accept_len, accept_slots, bonus_token, status, s);
 }
 
 const char* echo_status_string(int32_t code) {

@@ -33,176 +33,12 @@
 //                 partials in range order (deterministic) into out and lse.
 #include <hip/hip_ext.h>
 
+#include "attn_device.h"
 #include "echo_device.h"
 #include "echo_internal.h"
 
 namespace echo {
 namespace {
-
-constexpr int kD = ECHO_HEAD_DIM;   // 128
-constexpr int kThreads = 256;       // plan / combine workgroups
-constexpr int kWaves = 4;           // main kernel: waves (streams) per workgroup, one per CU
-constexpr int kMaxMT = 4;           // 16-row tiles per stream (394 of the 512 registers a wave has)
-constexpr int kPassRows = kMaxMT * 16;  // rows per stream (64)
-constexpr int kWaveStages = 2;      // per-wave LDS ring depth (32-key K+V tiles)
-constexpr int kTileKeys = 32;       // keys per tile
-constexpr int kMaskWords = 2;       // tree-tail mask words preloaded per row and segment
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.6931471805599453f;
-// The softmax reference max is raised only when a logit exceeds it by more than
-// 2^8 (in the exponent): probabilities stay <= 256, exact after normalisation.
-constexpr float kRescaleSlack = 8.0f;
-// A tile whose largest probability in a row exceeds this fraction of the
-// row's running sum also multiplies V by the bf16 residual p - bf16(p) (see
-// compute_tile).
-constexpr float kSplitFrac = 1.0f / 16.0f;
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-
-// One unit of the tile stream: a group of four streams of one request.
-// Stream s = 4 * group + w runs KV head s / passes over the rows of pass
-// s % passes; s >= hkv * passes is empty.
-struct Unit {
-  int32_t tile_start, tile_end;  // global tile range: ntail tail tiles, then prefix tiles
-  int32_t q0, nslots;            // the request's verify slots
-  int32_t kb, P;                 // KV prefix rows [kb, kb + P)
-  int32_t ntail, passes;         // ceil(nslots / 32); row passes per KV head
-  int32_t rpp, group;            // rows per pass (the last pass may have fewer); stream group
-  int32_t cut, pad;              // cut: covered by more than one workgroup
-};
-
-struct Cut {
-  int32_t unit, b0, b1, first_slot;  // workgroups b0..b1; partial slot of b0's segment
-  Unit u;                            // the unit itself (the merge needs no second lookup)
-};
-
-struct AttnWs {
-  int32_t* meta;   // [0] units, [1] tiles, [2] cut units, [3] workgroups with work
-  Unit* units;
-  int32_t* wg_unit;  // [nb] unit holding each workgroup's first tile
-  Cut* cuts;
-  float* part_ml;  // [2 * nb * 4 * 64][4]: reference max (log2 units), sum, rounded sum, 0
-  float* part_o;   // [2 * nb * 4 * 64][128]
-};
-
-__host__ __device__ inline size_t al(size_t x) { return (x + 255) / 256 * 256; }
-
-// Row passes of a request with fewer KV heads than a unit has waves: enough to
-// give every wave of its units a stream (see request_shape).
-__host__ __device__ inline int fill_passes(int hkv) { return (kWaves + hkv - 1) / hkv; }
-
-// Units never exceed one per request plus one per four streams; a request has at
-// most ceil(rows / 64) or fill_passes(hkv) passes per KV head.
-__host__ inline size_t unit_capacity(int R, int max_rows, int hq, int hkv) {
-  const size_t passes = size_t(R) * size_t(fill_passes(hkv)) +
-                        (size_t(max_rows) * (hq / hkv) + kPassRows - 1) / kPassRows;
-  return size_t(R) + (size_t(hkv) * passes + kWaves - 1) / kWaves;
-}
-
-__host__ __device__ inline size_t part_rows(int nb) {
-  return size_t(2) * nb * kWaves * kPassRows;
-}
-
-__host__ __device__ inline AttnWs attn_layout(void* base, size_t ucap, int nb) {
-  char* p = static_cast<char*>(base);
-  AttnWs w;
-  w.meta = reinterpret_cast<int32_t*>(p);
-  p += 256;
-  w.units = reinterpret_cast<Unit*>(p);
-  p += al(ucap * sizeof(Unit));
-  w.wg_unit = reinterpret_cast<int32_t*>(p);
-  p += al(size_t(nb) * sizeof(int32_t));
-  w.cuts = reinterpret_cast<Cut*>(p);
-  p += al(size_t(nb) * sizeof(Cut));
-  w.part_ml = reinterpret_cast<float*>(p);
-  p += al(part_rows(nb) * 4 * sizeof(float));
-  w.part_o = reinterpret_cast<float*>(p);
-  return w;
-}
-
-__host__ inline size_t attn_ws_total(size_t ucap, int nb) {
-  return 256 + al(ucap * sizeof(Unit)) + al(size_t(nb) * 4) + al(size_t(nb) * sizeof(Cut)) +
-         al(part_rows(nb) * 4 * 4) + al(part_rows(nb) * kD * 4);
-}
-
-// Partial row of (workgroup b, slot, stream w, row rho).
-__device__ __forceinline__ size_t part_row(int b, int slot, int w, int rho) {
-  return (size_t(2 * b + slot) * kWaves + w) * kPassRows + rho;
-}
-
-// floor(n / d) for 0 <= n < 2^42 and 0 < d < 2^31, without a 64-bit integer
-// division: the quotient through d's double reciprocal is within one of the
-// floor (the product's error is below 2^-9), and one integer step corrects it.
-struct DivBy {
-  long long d;
-  double inv;
-  __device__ explicit DivBy(long long d_) : d(d_), inv(1.0 / double(d_)) {}
-  __device__ __forceinline__ long long operator()(long long n) const {
-    long long q = static_cast<long long>(double(n) * inv);
-    if (q * d > n) --q;
-    else if ((q + 1) * d <= n) ++q;
-    return q;
-  }
-};
-
-// First tile of workgroup b when T tiles are cut into nw equal ranges (nw <= T).
-__device__ __forceinline__ long long range_lo(long long T, int b, int nw) { return T * b / nw; }
-__device__ __forceinline__ long long range_lo(long long T, int b, const DivBy& by_nw) {
-  return by_nw(T * b);
-}
-// Workgroup whose range holds tile t.
-__device__ __forceinline__ int range_of(long long t, long long T, int nw, const DivBy& by_t) {
-  return int(by_t((t + 1) * nw + T - 1)) - 1;
-}
-
-// The rows of stream w of a unit: KV head, first row and row count (rows == 0:
-// the stream is empty).
-struct Stream {
-  int kvh, row0, rows;
-};
-
-__device__ __forceinline__ Stream stream_of(const Unit& u, int w, int hkv, int G) {
-  Stream s = {0, 0, 0};
-  const int id = kWaves * u.group + w;
-  if (u.passes <= 0 || id >= hkv * u.passes) return s;
-  s.kvh = id / u.passes;
-  s.row0 = (id % u.passes) * u.rpp;
-  s.rows = min(u.rpp, u.nslots * G - s.row0);
-  return s;
-}
-
-// ---------------------------------------------------------------- plan ----
-// Where the requests' KV prefixes live: rows [kv_offsets[r], kv_offsets[r+1])
-// of a token-major cache, or (block_table != nullptr) prefix_len[r] positions
-// read through the request's row of the block table.
-struct KvSource {
-  const int64_t* kv_offsets;
-  long long kv_rows;
-  const int32_t* block_table;
-  const int32_t* prefix_len;
-  int page_size;
-  int max_pages;
-  long long num_pages;
-  const int32_t* page_bad;  // [R][page_chunks]: written by attn_pages, read by the plan
-  int page_chunks;
-};
-
-constexpr int kPageChunk = 256;  // page ids checked per attn_pages workgroup
-
-// Slot range and prefix extent of request r are usable (for a paged prefix:
-// its length fits its block-table row; the page ids are checked separately).
-__device__ __forceinline__ bool request_ok(const int32_t* q_offsets, const KvSource& kv,
-                                           int max_rows, int r) {
-  const int q0 = q_offsets[r], q1 = q_offsets[r + 1];
-  if (!(q0 >= 0 && q1 >= q0 && q1 <= max_rows)) return false;
-  if (kv.block_table == nullptr) {
-    const long long k0 = kv.kv_offsets[r], k1 = kv.kv_offsets[r + 1];
-    return k0 >= 0 && k1 >= k0 && k1 <= kv.kv_rows;
-  }
-  const long long P = kv.prefix_len[r];
-  return P >= 0 && P <= (long long)kv.max_pages * kv.page_size;
-}
 
 // Paged prefixes: workgroup (r, c) checks page ids c * 256 .. c * 256 + 255 of
 // request r and records whether one is outside [0, num_pages) (every chunk is
@@ -222,167 +58,10 @@ __global__ __launch_bounds__(kPageChunk) void attn_pages_kernel(KvSource kv) {
   if (threadIdx.x == 0) const_cast<int32_t*>(kv.page_bad)[size_t(r) * kv.page_chunks + c] = bad;
 }
 
-struct RequestShape {
-  int groups, tiles, q0, nsl, kb, P, ntail, passes, rpp;
-};
-
-// A request's rows per head split into passes of at most 64 rows, as even as
-// possible; its hkv * passes streams form ceil(/4) groups over the same tiles.
-// With fewer KV heads than a unit has waves (one KV head, or a tensor-parallel
-// share of a few), that would leave waves idle: the rows are then split into
-// fill_passes(hkv) passes (at least one row each), whose streams read the same
-// head's tiles and share them in the caches.
-// `ok` is request_ok of request r (evaluated once per plan).  A paged request's
-// kb is its index (its block table row), a contiguous one's its first row.
-__device__ __forceinline__ RequestShape request_shape(const int32_t* q_offsets, const KvSource& kv,
-                                                      bool ok, int R, int hkv, int G, int r) {
-  RequestShape s = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-  if (r >= R || !ok) return s;
-  s.q0 = q_offsets[r];
-  s.nsl = q_offsets[r + 1] - s.q0;
-  if (kv.block_table == nullptr) {
-    s.kb = int(kv.kv_offsets[r]);
-    s.P = int(kv.kv_offsets[r + 1] - kv.kv_offsets[r]);
-  } else {
-    s.kb = r;
-    s.P = kv.prefix_len[r];
-  }
-  const int rows = s.nsl * G;
-  s.passes = (rows + kPassRows - 1) / kPassRows;
-  if (s.passes == 0) return s;
-  s.passes = max(s.passes, min(rows, fill_passes(hkv)));
-  s.rpp = (rows + s.passes - 1) / s.passes;
-  s.ntail = (s.nsl + kTileKeys - 1) / kTileKeys;
-  s.groups = (hkv * s.passes + kWaves - 1) / kWaves;
-  s.tiles = s.ntail + (s.P + kTileKeys - 1) / kTileKeys;
-  return s;
-}
-
 __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
     const int32_t* __restrict__ q_offsets, KvSource kv, int R, int hkv, int G, int max_rows,
     int nb, long long ucap, AttnWs ws, int32_t* status) {
-  __shared__ int s_scan[kThreads / kWave + 1];
-  __shared__ int2 s_scan2[kThreads / kWave + 1];
-  __shared__ uint8_t s_ok[ECHO_MAX_REQUESTS + 1];
-  const int tid = threadIdx.x;
-  // one request per thread (R <= 256, the usual case): shapes and their scans
-  // are computed once and kept for pass B; the shape is taken with the same
-  // loads as the validity check
-  const bool single = R <= kThreads;
-  RequestShape s1 = {0, 0, 0, 0, 0, 0, 0, 0, 0};
-  int ub1 = 0, tb1 = 0;
-  int bits = 0;
-  for (int r = tid; r < R; r += kThreads) {
-    bool ok = request_ok(q_offsets, kv, max_rows, r);
-    if (kv.block_table != nullptr)
-      for (int c = 0; c < kv.page_chunks; ++c) ok = ok && kv.page_bad[size_t(r) * kv.page_chunks + c] == 0;
-    s_ok[r] = ok ? 1 : 0;
-    if (!ok) bits |= ECHO_DATA_BAD_OFFSETS;
-    if (single) s1 = request_shape(q_offsets, kv, ok, R, hkv, G, r);
-  }
-  __syncthreads();
-  auto ok_of = [&](int r) { return r < R && s_ok[r] != 0; };
-
-  // pass A: total units and tiles
-  long long T = 0, U = 0;
-  for (int base = 0; base < R; base += kThreads) {
-    const RequestShape s =
-        single ? s1 : request_shape(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
-    int tot_u, tot_t;
-    const int2 ex = block_exclusive_sum2<kThreads>(make_int2(s.groups, s.groups * s.tiles), s_scan2,
-                                                   &tot_u, &tot_t);
-    if (single) {
-      s1 = s;
-      ub1 = ex.x;
-      tb1 = ex.y;
-    }
-    U += tot_u;
-    T += tot_t;
-  }
-  // slot ranges that overlap (a non-monotone CSR) could ask for more units than
-  // the workspace holds, and tile indices are 32-bit: then nothing is scheduled
-  if (U > ucap || T > 0x7FFFFFFFll) {
-    if (tid == 0) {
-      bits |= ECHO_DATA_BAD_OFFSETS;
-      ws.meta[0] = 0;
-      ws.meta[1] = 0;
-      ws.meta[2] = 0;
-      ws.meta[3] = 0;
-    }
-    wave_status_or(status, bits);
-    return;
-  }
-  wave_status_or(status, bits);
-  // workgroups with work: never more than tiles, so that no range is empty
-  const int nw = T < nb ? int(T) : nb;
-  // pass B: units, the cut units and each workgroup's first unit
-  const DivBy by_t(T > 0 ? T : 1), by_nw(nw > 0 ? nw : 1);
-  int unit_run = 0, tile_run = 0, cut_run = 0;
-  for (int base = 0; base < R; base += kThreads) {
-    RequestShape s;
-    int ub, tb, tot_u, tot_t;
-    if (single) {
-      s = s1;
-      ub = ub1;
-      tb = tb1;
-      tot_u = int(U);
-      tot_t = int(T);
-    } else {
-      s = request_shape(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
-      const int2 ex = block_exclusive_sum2<kThreads>(make_int2(s.groups, s.groups * s.tiles),
-                                                     s_scan2, &tot_u, &tot_t);
-      ub = unit_run + ex.x;
-      tb = tile_run + ex.y;
-    }
-    // a unit is cut if two workgroup ranges share it
-    int ncut = 0;
-    for (int g = 0; g < s.groups; ++g) {
-      const long long ts = tb + g * s.tiles, te = ts + s.tiles;
-      if (range_of(ts, T, nw, by_t) != range_of(te - 1, T, nw, by_t)) ++ncut;
-    }
-    int tot_c;
-    const int cb = cut_run + block_exclusive_sum<kThreads>(ncut, s_scan, &tot_c);
-    int c = cb;
-    for (int g = 0; g < s.groups; ++g) {
-      Unit u;
-      u.tile_start = tb + g * s.tiles;
-      u.tile_end = u.tile_start + s.tiles;
-      u.q0 = s.q0;
-      u.nslots = s.nsl;
-      u.kb = s.kb;
-      u.P = s.P;
-      u.ntail = s.ntail;
-      u.passes = s.passes;
-      u.rpp = s.rpp;
-      u.group = g;
-      const int b0 = range_of(u.tile_start, T, nw, by_t), b1 = range_of(u.tile_end - 1, T, nw, by_t);
-      u.cut = b0 != b1;
-      u.pad = 0;
-      ws.units[ub + g] = u;
-      if (u.cut) {
-        Cut cu;
-        cu.unit = ub + g;
-        cu.b0 = b0;
-        cu.b1 = b1;
-        cu.first_slot = range_lo(T, b0, by_nw) < u.tile_start ? 1 : 0;
-        cu.u = u;
-        ws.cuts[c++] = cu;
-      }
-      // workgroups whose range starts inside this unit
-      int b = b0;
-      if (range_lo(T, b, by_nw) < u.tile_start) ++b;
-      for (; b <= b1; ++b) ws.wg_unit[b] = ub + g;
-    }
-    unit_run += tot_u;
-    tile_run += tot_t;
-    cut_run += tot_c;
-  }
-  if (tid == 0) {
-    ws.meta[0] = unit_run;
-    ws.meta[1] = int(T);
-    ws.meta[2] = cut_run;
-    ws.meta[3] = nw;
-  }
+  plan_body<kThreads>(q_offsets, kv, R, hkv, G, max_rows, nb, ucap, ws, status);
 }
 
 // ---------------------------------------------------------------- main ----
@@ -1302,7 +981,11 @@ size_t attn_workspace_bytes(int32_t R, int32_t max_rows, int32_t hq, int32_t hkv
   return attn_ws_total(unit_capacity(R, max_rows, hq, hkv), main_workgroups());
 }
 
-int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
+namespace {
+
+// The attention's launches; the plan (and a paged cache's page check) only if
+// `plan`, else the plan of the fused step's front kernel is in the workspace.
+int32_t launch_attn_impl(const AttnArgs& a, bool plan, hipStream_t stream) {
   (void)hipGetLastError();  // clear errors left by unrelated runtime calls
   const int nb = main_workgroups();
   const size_t ucap = unit_capacity(a.R, a.max_rows, a.hq, a.hkv);
@@ -1318,7 +1001,7 @@ int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
   kv.num_pages = static_cast<long long>(a.num_pages);
   kv.page_bad = nullptr;
   kv.page_chunks = 0;
-  if (a.block_table != nullptr) {
+  if (plan && a.block_table != nullptr) {
     // the flags borrow the start of the partials, which the main kernel only
     // writes later on the same stream
     kv.page_chunks = (a.max_pages + kPageChunk - 1) / kPageChunk;
@@ -1327,8 +1010,9 @@ int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
     hipLaunchKernelGGL(attn_pages_kernel, dim3(unsigned(a.R), unsigned(kv.page_chunks)),
                        dim3(kPageChunk), 0, stream, kv);
   }
-  hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kThreads), 0, stream, a.q_offsets, kv, a.R,
-                     a.hkv, G, a.max_rows, nb, static_cast<long long>(ucap), ws, a.status);
+  if (plan)
+    hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kThreads), 0, stream, a.q_offsets, kv, a.R,
+                       a.hkv, G, a.max_rows, nb, static_cast<long long>(ucap), ws, a.status);
   MainArgs m;
   m.q = a.q;
   m.k_new = a.k_new;
@@ -1360,6 +1044,16 @@ int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(nb * kCombineBlocks)), dim3(kThreads), 0,
                      stream, a.hq, a.hkv, G, ws, a.out, a.lse);
   return hipGetLastError() == hipSuccess ? ECHO_OK : ECHO_ERR_HIP;
+}
+
+}  // namespace
+
+int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
+  return launch_attn_impl(a, true, stream);
+}
+
+int32_t launch_tree_verify_attn_planned(const AttnArgs& a, hipStream_t stream) {
+  return launch_attn_impl(a, false, stream);
 }
 
 }  // namespace echo

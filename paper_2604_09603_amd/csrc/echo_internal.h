@@ -15,6 +15,12 @@ int32_t launch_gate(const int32_t* cand_offsets, const int32_t* parent, const fl
                     int32_t* num_selected, int32_t* trunc_depth, void* workspace, int32_t* status,
                     hipStream_t stream);
 size_t gate_workspace_bytes(int32_t R, int32_t N, int32_t budget);
+// The top-B gate without its last phase (gate_finish), which the fused step's
+// front kernel runs.
+int32_t launch_gate_select_only(const int32_t* cand_offsets, const int32_t* parent,
+                                const float* logq, int32_t R, int32_t N, int32_t budget,
+                                float* path_score, uint8_t* selected, int32_t* num_selected,
+                                void* workspace, int32_t* status, hipStream_t stream);
 
 // Path scores only (the first gate launch): per candidate the orderable key
 // (0 = never selectable), the clamped parent as a global index (-1: child of
@@ -81,6 +87,9 @@ struct AttnArgs {
   hipEvent_t ev_stop;
 };
 int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream);
+// The same without the plan: the fused step's front kernel wrote it into the
+// workspace (contiguous cache only).
+int32_t launch_tree_verify_attn_planned(const AttnArgs& a, hipStream_t stream);
 size_t attn_workspace_bytes(int32_t R, int32_t max_rows, int32_t hq, int32_t hkv);
 
 int32_t launch_accept(const int32_t* q_offsets, const int32_t* slot_parent,
@@ -103,5 +112,32 @@ int32_t launch_commit_kv(const int32_t* q_offsets, const int32_t* accept_len,
                          int32_t* prefix_len, int32_t* status, hipStream_t stream);
 
 int device_cu_count();
+
+// Fused step (front.hip): the gate's last phase, flatten & pack and the
+// attention plan (contiguous cache) in one single-workgroup launch, after
+// launch_gate_select_only and before launch_tree_verify_attn_planned.
+struct FrontLaunch {
+  int32_t N, R, budget, mask_words;
+  void* gate_workspace;
+  uint8_t* selected;
+  const int32_t* cand_offsets;
+  const int32_t* parent;
+  const int32_t* token;
+  const int32_t* root_token;
+  const int32_t* prefix_len;
+  int32_t* q_offsets;
+  int32_t* slot_cand;
+  int32_t* slot_parent;
+  int32_t* slot_token;
+  int32_t* position_ids;
+  uint32_t* tree_mask;
+  const int64_t* kv_offsets;
+  int64_t kv_rows;
+  int32_t max_rows, hq, hkv;
+  void* attn_workspace;
+  int32_t* status;
+};
+size_t front_lds_bytes(int32_t R, int32_t budget);
+int32_t launch_front(const FrontLaunch& f, hipStream_t stream);
 
 }  // namespace echo

@@ -3,7 +3,7 @@
 ``VerifyStep`` owns every input, output and workspace of a batch on one GPU
 (torch allocations, used only as device memory) and enqueues echo_gate ->
 echo_build_tree_mask -> echo_tree_verify_attn -> echo_accept on the current
-stream.  The target argmax per verify slot is an input of the last stage; the
+stream, or the same four stages as one echo_verify_step call (``run_fused``).  The target argmax per verify slot is an input of the last stage; the
 caller supplies it (``set_target``) because it comes from the target model.
 """
 import numpy as np
@@ -12,7 +12,7 @@ import torch
 from . import (HEAD_DIM, MAX_DEPTH, echo_accept, echo_accept_logits, echo_build_tree_mask,
                echo_commit_kv, echo_gate, echo_gate_elastic, echo_gate_sparse,
                echo_tree_verify_attn, echo_tree_verify_attn_paged,
-               echo_tree_verify_attn_paged_timed, echo_tree_verify_attn_timed,
+               echo_tree_verify_attn_paged_timed, echo_tree_verify_attn_timed, echo_verify_step,
                gate_elastic_workspace_size, gate_workspace_size, tree_verify_attn_workspace_size)
 
 
@@ -202,6 +202,26 @@ class VerifyStep:
                        self.k_new, self.v_new, self.R, self.cap, self.hkv, self.k_pages,
                        self.v_pages, self.page_size, self.block_table, self.cached_len,
                        status=self.status, stream=stream)
+
+    def fused_ok(self):
+        """The one-call step covers the top-B gate, a contiguous cache and acceptance
+        from target tokens."""
+        return (self.elastic is None and self.checkpoints is None and self.page_size is None
+                and not self.serve)
+
+    def run_fused(self, stream=None):
+        """The step as one echo_verify_step call (same outputs as run())."""
+        if not self.fused_ok():
+            raise ValueError("echo_verify_step covers the top-B gate on a contiguous cache")
+        echo_verify_step(self.cand_offsets, self.parent, self.logq, self.token, self.R, self.N,
+                         self.B, self.path_score, self.selected, self.num_selected, self.gate_ws,
+                         self.root_token, self.prefix_len, self.q_offsets, self.slot_cand,
+                         self.slot_parent, self.slot_token, self.position_ids, self.tree_mask,
+                         self.W, self.q, self.k_new, self.v_new, self.k_cache, self.v_cache,
+                         self.kv_offsets, self.kv_rows, self.cap, self.hq, self.hkv, self.D,
+                         self.sm_scale, self.out, self.lse, self.attn_ws, self.target_token,
+                         self.max_depth, self.accept_len, self.accept_slots, self.bonus_token,
+                         status=self.status, stream=stream)
 
     def run(self, stream=None, attn_events=None):
         self.gate(stream)

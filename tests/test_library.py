@@ -136,3 +136,46 @@ def test_attention_scale_and_timing_events_checked_on_host():
     assert probe(6, 1) == pkg.ERR_UNSUPPORTED
     assert probe(4, 0, P(264)) == pkg.ERR_INVALID_ARG
     assert probe(0, 0) == pkg.ERR_INVALID_ARG
+
+
+def test_verify_step_checked_on_host():
+    """echo_verify_step runs every check of the four calls before it launches
+    anything: each failing check gives that call's code (no GPU needed)."""
+    if not os.path.exists(pkg.LIB_PATH):
+        pytest.skip("libecho.so not built")
+    lib = pkg.load()
+    P = ctypes.c_void_p
+    R, N, B, W, cap = 1, 4, 4, 1, 5
+    gws = lib.echo_gate_workspace_size(R, N, B)
+    aws = lib.echo_tree_verify_attn_workspace_size(R, cap, 8, 8, 128)
+    base = dict(cand_offsets=P(256), parent=P(256), logq=P(256), token=P(256), R=R, N=N,
+                budget=B, path_score=None, selected=P(256), num_selected=P(256),
+                gate_ws=P(256), gate_ws_bytes=gws, root_token=P(256), prefix_len=P(256),
+                q_offsets=P(256), slot_cand=P(256), slot_parent=P(256), slot_token=P(256),
+                position_ids=P(256), tree_mask=P(256), mask_words=W, q=P(256), k_new=P(256),
+                v_new=P(256), k_cache=P(256), v_cache=P(256), kv_offsets=P(256), kv_rows=10,
+                max_rows=cap, hq=8, hkv=8, head_dim=128, scale=0.088, out=P(256), lse=None,
+                attn_ws=P(256), attn_ws_bytes=aws, target=P(256), max_depth=4,
+                accept_len=P(256), accept_slots=P(256), bonus=P(256), status=None, stream=None)
+
+    def step(**kw):
+        a = dict(base, **kw)
+        return lib.echo_verify_step(*a.values())
+
+    assert step(R=0) == pkg.ERR_INVALID_ARG
+    assert step(budget=16385) == pkg.ERR_UNSUPPORTED                 # ECHO_MAX_BUDGET + 1
+    assert step(token=None) == pkg.ERR_INVALID_ARG                  # the mask's tokens
+    assert step(gate_ws=P(257)) == pkg.ERR_WORKSPACE
+    assert step(gate_ws_bytes=gws - 1) == pkg.ERR_WORKSPACE
+    assert step(mask_words=0) == pkg.ERR_INVALID_ARG
+    assert step(tree_mask=None) == pkg.ERR_INVALID_ARG
+    assert step(head_dim=64) == pkg.ERR_UNSUPPORTED
+    assert step(hq=6, hkv=4) == pkg.ERR_INVALID_ARG
+    assert step(scale=-1.0) == pkg.ERR_INVALID_ARG
+    assert step(q=P(264)) == pkg.ERR_INVALID_ARG                     # not 16-byte aligned
+    assert step(attn_ws_bytes=aws - 1) == pkg.ERR_WORKSPACE
+    assert step(max_depth=0) == pkg.ERR_INVALID_ARG
+    assert step(max_depth=pkg.MAX_DEPTH + 1) == pkg.ERR_UNSUPPORTED
+    assert step(bonus=None) == pkg.ERR_INVALID_ARG
+    assert step(target=None) == pkg.ERR_INVALID_ARG
+    assert len(base) == 44
