@@ -161,18 +161,36 @@ struct KvSource {
 
 constexpr int kPageChunk = 256;  // page ids checked per attn_pages workgroup
 
-// Slot range and prefix extent of request r are usable (for a paged prefix:
-// its length fits its block-table row; the page ids are checked separately).
-__device__ __forceinline__ bool request_ok(const int32_t* q_offsets, const KvSource& kv,
-                                           int max_rows, int r) {
-  const int q0 = q_offsets[r], q1 = q_offsets[r + 1];
-  if (!(q0 >= 0 && q1 >= q0 && q1 <= max_rows)) return false;
+// What the plan reads of request r, loaded together: its slot range and its
+// prefix (a contiguous prefix's rows [k0, k1); a paged one's length P).
+struct RequestIn {
+  int q0, q1;
+  long long k0, k1, P;
+};
+
+__device__ __forceinline__ RequestIn load_request(const int32_t* q_offsets, const KvSource& kv,
+                                                  int r) {
+  RequestIn in;
+  in.q0 = q_offsets[r];
+  in.q1 = q_offsets[r + 1];
   if (kv.block_table == nullptr) {
-    const long long k0 = kv.kv_offsets[r], k1 = kv.kv_offsets[r + 1];
-    return k0 >= 0 && k1 >= k0 && k1 <= kv.kv_rows;
+    in.k0 = kv.kv_offsets[r];
+    in.k1 = kv.kv_offsets[r + 1];
+    in.P = in.k1 - in.k0;
+  } else {
+    in.k0 = 0;
+    in.k1 = 0;
+    in.P = kv.prefix_len[r];
   }
-  const long long P = kv.prefix_len[r];
-  return P >= 0 && P <= (long long)kv.max_pages * kv.page_size;
+  return in;
+}
+
+// Slot range and prefix extent of a request are usable (for a paged prefix: its
+// length fits its block-table row; the page ids are checked separately).
+__device__ __forceinline__ bool request_ok(const RequestIn& in, const KvSource& kv, int max_rows) {
+  if (!(in.q0 >= 0 && in.q1 >= in.q0 && in.q1 <= max_rows)) return false;
+  if (kv.block_table == nullptr) return in.k0 >= 0 && in.k1 >= in.k0 && in.k1 <= kv.kv_rows;
+  return in.P >= 0 && in.P <= (long long)kv.max_pages * kv.page_size;
 }
 
 struct RequestShape {
@@ -187,19 +205,14 @@ struct RequestShape {
 // head's tiles and share them in the caches.
 // `ok` is request_ok of request r (evaluated once per plan).  A paged request's
 // kb is its index (its block table row), a contiguous one's its first row.
-__device__ __forceinline__ RequestShape request_shape(const int32_t* q_offsets, const KvSource& kv,
+__device__ __forceinline__ RequestShape request_shape(const RequestIn& in, const KvSource& kv,
                                                       bool ok, int R, int hkv, int G, int r) {
   RequestShape s = {0, 0, 0, 0, 0, 0, 0, 0, 0};
   if (r >= R || !ok) return s;
-  s.q0 = q_offsets[r];
-  s.nsl = q_offsets[r + 1] - s.q0;
-  if (kv.block_table == nullptr) {
-    s.kb = int(kv.kv_offsets[r]);
-    s.P = int(kv.kv_offsets[r + 1] - kv.kv_offsets[r]);
-  } else {
-    s.kb = r;
-    s.P = kv.prefix_len[r];
-  }
+  s.q0 = in.q0;
+  s.nsl = in.q1 - in.q0;
+  s.kb = kv.block_table == nullptr ? int(in.k0) : r;
+  s.P = int(in.P);
   const int rows = s.nsl * G;
   s.passes = (rows + kPassRows - 1) / kPassRows;
   if (s.passes == 0) return s;
@@ -209,6 +222,14 @@ __device__ __forceinline__ RequestShape request_shape(const int32_t* q_offsets, 
   s.groups = (hkv * s.passes + kWaves - 1) / kWaves;
   s.tiles = s.ntail + (s.P + kTileKeys - 1) / kTileKeys;
   return s;
+}
+
+// request_shape of request r, its fields loaded here (r < R).
+__device__ __forceinline__ RequestShape request_shape_at(const int32_t* q_offsets,
+                                                         const KvSource& kv, bool ok, int R,
+                                                         int hkv, int G, int r) {
+  if (r >= R || !ok) return RequestShape{0, 0, 0, 0, 0, 0, 0, 0, 0};
+  return request_shape(load_request(q_offsets, kv, r), kv, ok, R, hkv, G, r);
 }
 
 // The plan on one workgroup of NT threads (see attn_plan above): the units,
@@ -230,12 +251,13 @@ __device__ void plan_body(const int32_t* __restrict__ q_offsets, const KvSource&
   int ub1 = 0, tb1 = 0;
   int bits = 0;
   for (int r = tid; r < R; r += NT) {
-    bool ok = request_ok(q_offsets, kv, max_rows, r);
+    const RequestIn in = load_request(q_offsets, kv, r);
+    bool ok = request_ok(in, kv, max_rows);
     if (kv.block_table != nullptr)
       for (int c = 0; c < kv.page_chunks; ++c) ok = ok && kv.page_bad[size_t(r) * kv.page_chunks + c] == 0;
     s_ok[r] = ok ? 1 : 0;
     if (!ok) bits |= ECHO_DATA_BAD_OFFSETS;
-    if (single) s1 = request_shape(q_offsets, kv, ok, R, hkv, G, r);
+    if (single) s1 = request_shape(in, kv, ok, R, hkv, G, r);
   }
   __syncthreads();
   auto ok_of = [&](int r) { return r < R && s_ok[r] != 0; };
@@ -244,7 +266,7 @@ __device__ void plan_body(const int32_t* __restrict__ q_offsets, const KvSource&
   long long T = 0, U = 0;
   for (int base = 0; base < R; base += NT) {
     const RequestShape s =
-        single ? s1 : request_shape(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
+        single ? s1 : request_shape_at(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
     int tot_u, tot_t;
     const int2 ex = block_exclusive_sum2<NT>(make_int2(s.groups, s.groups * s.tiles), s_scan2,
                                                    &tot_u, &tot_t);
@@ -285,7 +307,7 @@ __device__ void plan_body(const int32_t* __restrict__ q_offsets, const KvSource&
       tot_u = int(U);
       tot_t = int(T);
     } else {
-      s = request_shape(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
+      s = request_shape_at(q_offsets, kv, ok_of(base + tid), R, hkv, G, base + tid);
       const int2 ex = block_exclusive_sum2<NT>(make_int2(s.groups, s.groups * s.tiles),
                                                      s_scan2, &tot_u, &tot_t);
       ub = unit_run + ex.x;

@@ -125,11 +125,11 @@ __device__ __forceinline__ int add_by_depth(bool on, int d, int* counter) {
   int before = 0;
   while (rem != 0ull) {  // uniform: one round per distinct depth
     const int lead = __builtin_ctzll(rem);
-    const int dl = __shfl(d, lead, kWave);
+    const int dl = __builtin_amdgcn_readlane(d, lead);
     const uint64_t bal = __ballot(on && d == dl);
     int base = 0;
     if ((threadIdx.x & (kWave - 1)) == lead) base = atomicAdd(&counter[dl], __popcll(bal));
-    base = __shfl(base, lead, kWave);
+    base = __builtin_amdgcn_readlane(base, lead);
     if (on && d == dl) before = base + lanes_below(bal);
     rem &= ~bal;
   }
@@ -146,15 +146,13 @@ __device__ __forceinline__ void append_wave(bool take, int i, uint32_t k, int* c
   if (bal == 0ull) return;  // uniform
   const int lane = threadIdx.x & (kWave - 1);
   const int n = __popcll(bal);
-  uint32_t km = take ? k : 0u;
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) km = max(km, uint32_t(__shfl_xor(int(km), off, kWave)));
+  const uint32_t km = wave_max(take ? k : 0u);
   int base = 0;
   if (lane == 0) {
     base = atomicAdd(cnt, n);
     atomicMax(mx, km);
   }
-  base = __shfl(base, 0, kWave);
+  base = __builtin_amdgcn_readlane(base, 0);
   if (take) {
     const int pos = base + lanes_below(bal);
     list[pos] = i;
@@ -251,12 +249,7 @@ __device__ void trajectory_staged(int r, int lo, int n, const GateScoreBufs& sb,
   }
   __syncthreads();
   if (tid < kWave) {  // inclusive scan of the depth counts (18 entries) in one wave
-    int v = tid <= kSlots ? L.off[tid] : 0;
-#pragma unroll
-    for (int o = 1; o < 32; o <<= 1) {
-      const int u = __shfl_up(v, o, kWave);
-      if (tid >= o) v += u;
-    }
+    const int v = wave_inclusive_sum(tid <= kSlots ? L.off[tid] : 0);
     if (tid <= kSlots) L.off[tid] = v;
   }
   __syncthreads();
@@ -401,8 +394,7 @@ __global__ __launch_bounds__(kFinThreads) void elastic_finish_kernel(int R, int 
     int v = 0;
 #pragma unroll
     for (int k = 0; k < kFinThreads / kWave; ++k) v += s_tot[lane + kWave * k][d];
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+    v = int(wave_sum(uint32_t(v)));
     if (lane == 0) s_col[d] = v;
   }
   __syncthreads();

@@ -1,8 +1,8 @@
 // The fused step's front kernel: the last phase of the top-B gate (eq. 4),
 // flatten & pack (Fig. 3, stage 3) and the attention plan, one after another
 // on one workgroup.  Each of the three is one workgroup that waits for the one
-// before it; as separate launches each spends 3-4 us starting (waves launched,
-// code and arguments fetched, first loads) before its work.
+// before it, so as separate launches the step pays a kernel boundary (one
+// kernel's drain, the next one's launch) between each pair.
 //
 // The three phases share one dynamic LDS buffer: the gate's gathered
 // candidates (2 x 32 KB and the select blocks' offsets) first, then the mask's
@@ -57,14 +57,17 @@ struct FrontArgs {
 template <bool kAligned>
 __global__ __launch_bounds__(kFrontThreads) void front_kernel(FrontArgs a) {
   extern __shared__ int32_t smem[];
+  // The request tables of flatten & pack are loaded first, into registers, so
+  // that their memory latency passes with that of the gate's first loads.
+  const MaskTables tab = load_mask_tables(a.cand_offsets, a.root_token, a.prefix_len, a.R);
   if (a.N > 0)  // as the gate call, which skips its last phase without candidates
     gate_finish_body(a.N, a.nblocks, a.gws, a.selected, a.status,
                      FinishLds{reinterpret_cast<uint32_t*>(smem), smem + kSortCap,
                                smem + 2 * kSortCap});
   __syncthreads();
-  mask_body<kAligned>(a.cand_offsets, a.parent, a.token, a.selected, a.root_token, a.prefix_len,
-                      a.R, a.N, a.budget, a.q_offsets, a.slot_cand, a.slot_parent, a.slot_token,
-                      a.position_ids, a.tree_mask, a.W, a.status, smem);
+  mask_body<kAligned>(tab, a.parent, a.token, a.selected, a.R, a.N, a.budget, a.q_offsets,
+                      a.slot_cand, a.slot_parent, a.slot_token, a.position_ids, a.tree_mask, a.W,
+                      a.status, smem);
   if (!a.plan) return;
   __syncthreads();
   plan_body<kFrontThreads>(a.q_offsets, a.kv, a.R, a.hkv, a.G, a.max_rows, a.nb, a.ucap, a.aws,

@@ -49,11 +49,8 @@ __device__ void write_block_hist(const uint32_t* s_hist, uint2* s_red, GateWs& w
     fin += c;
     if (c != 0u) top = max(top, uint32_t(i + 1));
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    fin += __shfl_xor(fin, off, kWave);
-    top = max(top, uint32_t(__shfl_xor(top, off, kWave)));
-  }
+  fin = wave_sum(fin);
+  top = wave_max(top);
   if ((threadIdx.x & (kWave - 1)) == 0) s_red[threadIdx.x / kWave] = make_uint2(fin, top);
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -302,11 +299,8 @@ __device__ BinResult find_bin(int nblocks, int budget, const GateWs& ws, bool re
     fin += v.x;
     top = max(top, v.y);
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    fin += __shfl_xor(fin, off, kWave);
-    top = max(top, uint32_t(__shfl_xor(top, off, kWave)));
-  }
+  fin = wave_sum(fin);
+  top = wave_max(top);
   if (lane == 0) s_red[t / kWave] = make_uint2(fin, top);
   __syncthreads();
   fin = 0u;
@@ -343,12 +337,7 @@ __device__ BinResult find_bin(int nblocks, int budget, const GateWs& ws, bool re
         uint32_t cnt = 0u;
 #pragma unroll
         for (int g = 0; g < kChunkGroups; ++g) cnt += s_part[g][t];
-        uint32_t incl = cnt;  // inclusive sum over bins hi .. hi - t
-#pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-          const uint32_t u = __shfl_up(incl, off, kWave);
-          if (t >= off) incl += u;
-        }
+        const uint32_t incl = wave_scan(cnt, 0u, AddOp{});  // sum over bins hi .. hi - t
         const uint32_t above = s_state[0];
         const bool cross = above + incl >= m && above + incl - cnt < m;
         if (cross) {
@@ -357,7 +346,7 @@ __device__ BinResult find_bin(int nblocks, int budget, const GateWs& ws, bool re
           s_res.need = m - (above + incl - cnt);
           s_state[1] = 1u;
         }
-        const uint32_t total = __shfl(incl, kWave - 1, kWave);
+        const uint32_t total = uint32_t(__builtin_amdgcn_readlane(int(incl), kWave - 1));
         if (t == 0) s_state[0] = above + total;
       }
       __syncthreads();

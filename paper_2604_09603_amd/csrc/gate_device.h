@@ -108,12 +108,7 @@ __device__ __forceinline__ void digit_search(const uint32_t* h, uint32_t need, i
     c[j] = h[255 - 4 * lane - j];
     sum += c[j];
   }
-  uint32_t incl = sum;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const uint32_t u = __shfl_up(incl, off, kWave);
-    if (lane >= off) incl += u;
-  }
+  const uint32_t incl = wave_scan(sum, 0u, AddOp{});
   const unsigned long long hit = __ballot(incl >= need);
   const int l0 = hit != 0ull ? __builtin_ctzll(hit) : 0;
   if (lane == l0) {
@@ -214,6 +209,8 @@ __device__ void gate_finish_body(int N, int nblocks, const GateWs& ws,
   int* s_base = lds.s_base;
   __shared__ int s_scan[kGateThreads / kWave + 1];
   __shared__ RadixLds s_rl;
+  // the first kGateThreads block counts are loaded with the selection's size
+  const int c_first = int(threadIdx.x) < nblocks ? int(ws.ccount[threadIdx.x]) : 0;
   const GateMeta mt = *ws.meta;
   const uint32_t m = uint32_t(mt.num_selected);
   if (m == 0u) return;
@@ -222,7 +219,7 @@ __device__ void gate_finish_body(int N, int nblocks, const GateWs& ws,
   int run = 0;
   for (int b0 = 0; b0 < nblocks; b0 += kGateThreads) {
     const int b = b0 + threadIdx.x;
-    const int c = b < nblocks ? int(ws.ccount[b]) : 0;
+    const int c = b0 == 0 ? c_first : (b < nblocks ? int(ws.ccount[b]) : 0);
     int tot;
     const int ex = block_exclusive_sum<kGateThreads>(c, s_scan, &tot);
     if (b < nblocks && b < kGateThreads) s_base[b] = run + ex;

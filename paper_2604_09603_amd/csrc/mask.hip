@@ -31,9 +31,9 @@ __global__ __launch_bounds__(kMaskThreads) void mask_kernel(
     int32_t* __restrict__ position_ids, uint32_t* __restrict__ tree_mask, int W,
     int32_t* status) {
   extern __shared__ int32_t smem[];
-  mask_body<kAligned>(cand_offsets, parent, token, selected, root_token, prefix_len, R, N, budget,
-                      q_offsets, slot_cand, slot_parent, slot_token, position_ids, tree_mask, W,
-                      status, smem);
+  const MaskTables tab = load_mask_tables(cand_offsets, root_token, prefix_len, R);
+  mask_body<kAligned>(tab, parent, token, selected, R, N, budget, q_offsets, slot_cand,
+                      slot_parent, slot_token, position_ids, tree_mask, W, status, smem);
 }
 
 }  // namespace
