@@ -30,8 +30,11 @@ FLAGS = [
 #   maxima) is preceded by a v_max_f32 x, x, x that quiets signalling NaNs,
 #   about 50 extra VALU instructions per 64-row tile.  Infinities (masked keys
 #   are -inf) keep their meaning; NaN inputs give unspecified outputs.
+# The fused step's tail kernel holds the attention's combine and is built the
+# same way, so that its merges are the combine launch's to the bit.
 FILE_FLAGS = {
     "attn.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1", "-fno-honor-nans"],
+    "tail.hip": ["-mllvm", "--amdgpu-mfma-vgpr-form=1", "-fno-honor-nans"],
 }
 
 

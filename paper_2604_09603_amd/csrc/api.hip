@@ -424,12 +424,13 @@ int32_t echo_verify_step(
   f.status = status;
   rc = echo::launch_front(f, s);
   if (rc != ECHO_OK) return rc;
-  if (max_rows > 0) {
-    rc = echo::launch_tree_verify_attn_planned(a, s);
-    if (rc != ECHO_OK) return rc;
-  }
-  return echo::launch_accept(q_offsets, slot_parent, slot_token, target_token, R, max_rows,
-                             max_depth, accept_len, accept_slots, bonus_token, status, s);
+  if (max_rows == 0)  // no attention rows: the acceptance alone
+    return echo::launch_accept(q_offsets, slot_parent, slot_token, target_token, R, max_rows,
+                               max_depth, accept_len, accept_slots, bonus_token, status, s);
+  rc = echo::launch_tree_verify_attn_main(a, s);
+  if (rc != ECHO_OK) return rc;
+  return echo::launch_tail(a, slot_parent, slot_token, target_token, max_depth, accept_len,
+                           accept_slots, bonus_token, s);
 }
 
 const char* echo_status_string(int32_t code) {

@@ -821,156 +821,10 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
 }
 
 // ------------------------------------------------------------- combine ----
-// One thread per (cut unit, stream, pair of rows, 4 dims): rows rho and
-// rho + 32 of the stream; a cut's items span kCombineBlocks workgroups.  The
-// partials are merged in workgroup order.
-constexpr int kCombineRowsPerThread = 2;
-constexpr int kCombineItems = kWaves * (kPassRows / kCombineRowsPerThread) * (kD / 4);
-constexpr int kCombineBlocks = kCombineItems / kThreads;
-constexpr int kFastParts = 4;  // cuts over at most this many workgroups merge in one round trip
-static_assert(kCombineItems % kThreads == 0, "combine tiling");
-
-// One output row (4 dims) and its LSE from the partials of its parts: (max,
-// sum, rounded sum) and O of each (parts with max -inf are absent or empty).
-template <int NP>
-__device__ __forceinline__ void merge_parts(const floatx4 (&ml)[NP], const floatx4 (&po)[NP],
-                                            int np, float* o, float* l) {
-  float M = -__builtin_inff();
-#pragma unroll
-  for (int i = 0; i < NP; ++i)
-    if (i < np) M = fmaxf(M, ml[i][0]);
-  float L = 0.0f, Lq = 0.0f;
-  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (M != -__builtin_inff()) {
-#pragma unroll
-    for (int i = 0; i < NP; ++i) {
-      if (i >= np || ml[i][0] == -__builtin_inff()) continue;
-      const float wgt = __builtin_amdgcn_exp2f(ml[i][0] - M);
-      L += wgt * ml[i][1];
-      Lq += wgt * ml[i][2];
-      acc += wgt * po[i];
-    }
-  }
-  const float inv = Lq > 0.0f ? 1.0f / Lq : 0.0f;
-  __builtin_nontemporal_store(acc * inv, reinterpret_cast<floatx4*>(o));
-  if (l != nullptr) *l = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
-}
-
 __global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv, int G, AttnWs ws,
                                                                 float* __restrict__ out,
                                                                 float* __restrict__ lse) {
-  const int ci = blockIdx.x / kCombineBlocks;
-  if (ci >= ws.meta[2]) return;
-  const int e = (blockIdx.x % kCombineBlocks) * kThreads + threadIdx.x;
-  constexpr int kRowSpan = kPassRows / kCombineRowsPerThread;
-  constexpr int NR = kCombineRowsPerThread;
-  const int w = e / (kRowSpan * (kD / 4));
-  const int rho0 = (e / (kD / 4)) % kRowSpan;
-  const int d4 = (e % (kD / 4)) * 4;
-  const Cut c = ws.cuts[ci];
-  const Unit& u = c.u;
-  const Stream sm = stream_of(u, w, hkv, G);
-  if (rho0 >= sm.rows) return;
-  const int nparts = c.b1 - c.b0 + 1;
-  // partial of part i: workgroup b0 + i, whose segment may sit in its second slot
-  auto prow_of = [&](int i, int rho) {
-    return part_row(c.b0 + i, i == 0 ? c.first_slot : 0, w, rho);
-  };
-  auto out_row = [&](int rho) {
-    const int ra = sm.row0 + rho;
-    return size_t(u.q0 + ra / G) * hq + sm.kvh * G + ra % G;
-  };
-  if (nparts <= kFastParts) {
-    // every load of both rows issued at once: one memory round trip
-    floatx4 ml[NR][kFastParts], po[NR][kFastParts];
-#pragma unroll
-    for (int k = 0; k < NR; ++k) {
-      const int rho = rho0 + k * kRowSpan;
-#pragma unroll
-      for (int i = 0; i < kFastParts; ++i) {
-        ml[k][i] = floatx4{-__builtin_inff(), 0.0f, 0.0f, 0.0f};
-        po[k][i] = floatx4{0.f, 0.f, 0.f, 0.f};
-        if (i < nparts && rho < sm.rows) {
-          const size_t prow = prow_of(i, rho);
-          ml[k][i] = *reinterpret_cast<const floatx4*>(ws.part_ml + prow * 4);
-          po[k][i] = *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
-        }
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < NR; ++k) {
-      const int rho = rho0 + k * kRowSpan;
-      if (rho >= sm.rows) continue;
-      const size_t orow = out_row(rho);
-      merge_parts<kFastParts>(ml[k], po[k], nparts, out + orow * kD + d4,
-                              lse != nullptr && d4 == 0 ? lse + orow : nullptr);
-    }
-    return;
-  }
-  // more parts: kFastParts at a time for both rows, in order (the same arithmetic
-  // as the fast path; two memory round trips per batch instead of two per part)
-  float M[NR], L[NR], Lq[NR];
-  floatx4 acc[NR];
-#pragma unroll
-  for (int k = 0; k < NR; ++k) {
-    M[k] = -__builtin_inff();
-    L[k] = 0.0f;
-    Lq[k] = 0.0f;
-    acc[k] = floatx4{0.f, 0.f, 0.f, 0.f};
-  }
-  for (int i0 = 0; i0 < nparts; i0 += kFastParts) {
-    float mb[NR][kFastParts];
-#pragma unroll
-    for (int k = 0; k < NR; ++k)
-#pragma unroll
-      for (int j = 0; j < kFastParts; ++j) {
-        const int rho = rho0 + k * kRowSpan;
-        mb[k][j] = i0 + j < nparts && rho < sm.rows ? ws.part_ml[prow_of(i0 + j, rho) * 4]
-                                                    : -__builtin_inff();
-      }
-#pragma unroll
-    for (int k = 0; k < NR; ++k)
-#pragma unroll
-      for (int j = 0; j < kFastParts; ++j) M[k] = fmaxf(M[k], mb[k][j]);
-  }
-  for (int i0 = 0; i0 < nparts; i0 += kFastParts) {
-    floatx4 ml[NR][kFastParts], po[NR][kFastParts];
-#pragma unroll
-    for (int k = 0; k < NR; ++k)
-#pragma unroll
-      for (int j = 0; j < kFastParts; ++j) {
-        const int rho = rho0 + k * kRowSpan;
-        ml[k][j] = floatx4{-__builtin_inff(), 0.0f, 0.0f, 0.0f};
-        po[k][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-        if (i0 + j < nparts && rho < sm.rows) {
-          const size_t prow = prow_of(i0 + j, rho);
-          ml[k][j] = *reinterpret_cast<const floatx4*>(ws.part_ml + prow * 4);
-          po[k][j] = *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
-        }
-      }
-#pragma unroll
-    for (int k = 0; k < NR; ++k) {
-      if (M[k] == -__builtin_inff()) continue;
-#pragma unroll
-      for (int j = 0; j < kFastParts; ++j) {
-        if (ml[k][j][0] == -__builtin_inff()) continue;
-        const float wgt = __builtin_amdgcn_exp2f(ml[k][j][0] - M[k]);
-        L[k] += wgt * ml[k][j][1];
-        Lq[k] += wgt * ml[k][j][2];
-        acc[k] += wgt * po[k][j];
-      }
-    }
-  }
-#pragma unroll
-  for (int k = 0; k < NR; ++k) {
-    const int rho = rho0 + k * kRowSpan;
-    if (rho >= sm.rows) continue;
-    const size_t orow = out_row(rho);
-    const float inv = Lq[k] > 0.0f ? 1.0f / Lq[k] : 0.0f;
-    __builtin_nontemporal_store(acc[k] * inv, reinterpret_cast<floatx4*>(out + orow * kD + d4));
-    if (lse != nullptr && d4 == 0)
-      lse[orow] = L[k] > 0.0f ? (M[k] + log2f(L[k])) * kLn2 : -__builtin_inff();
-  }
+  combine_body(hq, hkv, G, ws, out, lse, blockIdx.x);
 }
 
 int main_workgroups() { return device_cu_count(); }
@@ -984,8 +838,9 @@ size_t attn_workspace_bytes(int32_t R, int32_t max_rows, int32_t hq, int32_t hkv
 namespace {
 
 // The attention's launches; the plan (and a paged cache's page check) only if
-// `plan`, else the plan of the fused step's front kernel is in the workspace.
-int32_t launch_attn_impl(const AttnArgs& a, bool plan, hipStream_t stream) {
+// `plan`, else the plan of the fused step's front kernel is in the workspace;
+// the combine only if `combine`, else the fused step's tail kernel runs it.
+int32_t launch_attn_impl(const AttnArgs& a, bool plan, bool combine, hipStream_t stream) {
   (void)hipGetLastError();  // clear errors left by unrelated runtime calls
   const int nb = main_workgroups();
   const size_t ucap = unit_capacity(a.R, a.max_rows, a.hq, a.hkv);
@@ -1041,19 +896,20 @@ int32_t launch_attn_impl(const AttnArgs& a, bool plan, hipStream_t stream) {
                          0) != hipSuccess)
     return ECHO_ERR_HIP;
   // cut units number fewer than the main kernel's workgroups
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(nb * kCombineBlocks)), dim3(kThreads), 0,
-                     stream, a.hq, a.hkv, G, ws, a.out, a.lse);
+  if (combine)
+    hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(nb * kCombineBlocks)), dim3(kThreads), 0,
+                       stream, a.hq, a.hkv, G, ws, a.out, a.lse);
   return hipGetLastError() == hipSuccess ? ECHO_OK : ECHO_ERR_HIP;
 }
 
 }  // namespace
 
 int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream) {
-  return launch_attn_impl(a, true, stream);
+  return launch_attn_impl(a, true, true, stream);
 }
 
-int32_t launch_tree_verify_attn_planned(const AttnArgs& a, hipStream_t stream) {
-  return launch_attn_impl(a, false, stream);
+int32_t launch_tree_verify_attn_main(const AttnArgs& a, hipStream_t stream) {
+  return launch_attn_impl(a, false, false, stream);
 }
 
 }  // namespace echo

@@ -87,9 +87,9 @@ struct AttnArgs {
   hipEvent_t ev_stop;
 };
 int32_t launch_tree_verify_attn(const AttnArgs& a, hipStream_t stream);
-// The same without the plan: the fused step's front kernel wrote it into the
-// workspace (contiguous cache only).
-int32_t launch_tree_verify_attn_planned(const AttnArgs& a, hipStream_t stream);
+// The main kernel alone: the fused step's front kernel wrote the plan into the
+// workspace (contiguous cache only) and its tail kernel runs the combine.
+int32_t launch_tree_verify_attn_main(const AttnArgs& a, hipStream_t stream);
 size_t attn_workspace_bytes(int32_t R, int32_t max_rows, int32_t hq, int32_t hkv);
 
 int32_t launch_accept(const int32_t* q_offsets, const int32_t* slot_parent,
@@ -115,7 +115,7 @@ int device_cu_count();
 
 // Fused step (front.hip): the gate's last phase, flatten & pack and the
 // attention plan (contiguous cache) in one single-workgroup launch, after
-// launch_gate_select_only and before launch_tree_verify_attn_planned.
+// launch_gate_select_only and before launch_tree_verify_attn_main.
 struct FrontLaunch {
   int32_t N, R, budget, mask_words;
   void* gate_workspace;
@@ -139,5 +139,11 @@ struct FrontLaunch {
 };
 size_t front_lds_bytes(int32_t R, int32_t budget);
 int32_t launch_front(const FrontLaunch& f, hipStream_t stream);
+
+// Fused step (tail.hip): the attention's combine and the greedy acceptance in
+// one launch, after launch_tree_verify_attn_main; `a` as for that call.
+int32_t launch_tail(const AttnArgs& a, const int32_t* slot_parent, const int32_t* slot_token,
+                    const int32_t* target_token, int32_t max_depth, int32_t* accept_len,
+                    int32_t* accept_slots, int32_t* bonus_token, hipStream_t stream);
 
 }  // namespace echo

@@ -142,3 +142,13 @@ def test_fused_step_invalid_data_and_empty_requests():
                 logq=np.array([-0.1, -0.2, -0.3, -0.4, -0.1, -0.5, -0.2], np.float32),
                 root_token=np.array([0, 1, 2, 0], np.int32))
     _compare(make_micro_batch(pool, 5, hq=8, hkv=4, p_range=(0, 0)))
+
+
+def test_fused_step_long_requests():
+    """Requests with more verify slots than the tail kernel stages in LDS (256):
+    its acceptance reads them from memory, the acceptance launch from LDS."""
+    rng = np.random.default_rng(23)
+    pool = synth.micro_pool(rng, 3, 700, p_neg_inf=0.0)
+    _log("[fused] long requests")
+    res = _compare(make_micro_batch(pool, 1200, hq=8, hkv=2, p_range=(0, 40), seed=9))
+    assert int(np.diff(res["q_offsets"]).max()) > 256
