@@ -318,10 +318,11 @@ int32_t echo_accept(const int32_t* q_offsets, const int32_t* slot_parent,
  * mask's unused workspace is dropped, `token` is the mask's candidate tokens,
  * `max_rows` serves the attention and the acceptance) and bit-identical
  * outputs and status bits.  It runs the gate's last phase, flatten & pack and
- * the attention's plan in one single-workgroup launch: the three are one
- * workgroup each and run back to back, and as separate launches each spends
- * 3-4 us starting before its first data arrives.  Every check of the four
- * calls runs before anything is launched; a failing check launches nothing.
+ * the attention's plan in one single-workgroup launch (the three are one
+ * workgroup each and run back to back), and the acceptance inside the
+ * attention's combine launch (it reads nothing the attention writes): five
+ * launches instead of eight.  Every check of the four calls runs before
+ * anything is launched; a failing check launches nothing.
  * Needs mask_words * 32 >= budget + 1 and the same LDS bound as the mask
  * call (ECHO_ERR_UNSUPPORTED beyond it).
  */
