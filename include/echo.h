@@ -238,8 +238,11 @@ size_t echo_build_tree_mask_workspace_size(int32_t R, int32_t N, int32_t budget)
  * rows).  Where one key of a 32-key tile may carry more than 1/16 of a row's
  * weight so far, the bf16 residual p - bf16(p) enters a second product, so
  * that rows whose weight sits on a few keys keep 2^-17 of relative error on
- * those weights; elsewhere each weight is within 2^-9 of itself.  The LSE
- * uses the fp32 sum.  NaN inputs give unspecified outputs.
+ * those weights; elsewhere each weight is within 2^-9 of itself.  A row whose
+ * keys are split between workgroups is merged from partial outputs stored in
+ * fp16 with a power-of-two scale per row (rounding: 2^-12 of the row's largest
+ * partial value).  The LSE uses the fp32 sum.  NaN inputs give unspecified
+ * outputs.
  *   q        [max_rows][Hq][128]  bf16 (slot-indexed, RoPE already applied)
  *   k_new, v_new [max_rows][Hkv][128] bf16 (K/V of the verify slots)
  *   k_cache, v_cache [kv_rows][Hkv][128] bf16, token-major (request r's prefix

@@ -635,14 +635,34 @@ __device__ __forceinline__ uint32_t mask_word(const MainArgs& a, const Unit& ud,
              : 0u;
 }
 
+// Dims 16 (2j) + 4 g + [0, 4) and 16 (2j + 1) + 4 g + [0, 4) of a lane's row,
+// scaled and rounded to fp16: one 16-byte store (see part_dim).
+__device__ __forceinline__ halfx8 pack_part(floatx4 lo4, floatx4 hi4, float sc) {
+  const halfx4 a0 = __builtin_convertvector(lo4 * sc, halfx4);
+  const halfx4 a1 = __builtin_convertvector(hi4 * sc, halfx4);
+  return halfx8{a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+}
+
+// The partial of a workgroup's first segment when its unit is cut and more
+// segments follow: the next segment's first loads would wait for its stores,
+// which drain slowly while every workgroup streams the cache (14 us at q235b),
+// so it is held in registers and stored after the workgroup's last segment.
+struct HeldPartial {
+  uint32_t h[kMaxMT][16];  // the rows in fp16, packed as the stores write them
+  floatx4 ml[kMaxMT];      // max, sum, rounded sum and scale exponent of the lane's row
+  int mt, rows;            // row tiles held; rows of the stream
+  size_t prow0;            // partial row of the stream's row 0
+};
+
 // The wave's stream over one unit segment [seg_lo, seg_hi), then its output
-// (final or partial).
+// (final, partial, or, when `held` (wave-uniform), a partial kept in `hold`).
 template <int MT>
 __device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws, const Unit& ud,
                                             const Stream& sm, int seg_lo, int seg_hi, int lo,
                                             int hi, int nunits, int b, const char* ring,
                                             uint32_t ring_lds, Issuer& is,
-                                            const CopyPlan& cp, const LaneOffsets& lof) {
+                                            const CopyPlan& cp, const LaneOffsets& lof,
+                                            bool held, HeldPartial& hold) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wid = wave_id();
   const int lr = lane & 15, lg = lane >> 4;
@@ -732,11 +752,28 @@ __device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws,
   // ---- output of the segment ----
   const bool cut = ud.cut != 0;
   const int slot_id = lo < ud.tile_start ? 1 : 0;
+  if (held) {
+    hold.mt = MT;
+    hold.rows = sm.rows;
+    hold.prow0 = part_row(b, slot_id, wid, 0);
+  }
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
     const float L = row_sum4(rt[i].l);
     const float Lq = row_sum4(rt[i].lq);
     const float M = rt[i].m;
+    // a cut unit's partial row goes out in fp16, scaled by 2^-e so that its
+    // largest magnitude lies in [2^14, 2^15): half the bytes of fp32
+    int e = 0;
+    if (cut) {
+      float mx = 0.0f;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) mx = fmaxf(mx, fabsf(rt[i].o[dt][c]));
+      mx = row_max4(mx);
+      e = mx > 0.0f ? __builtin_amdgcn_frexp_expf(mx) - 15 : 0;
+    }
     const int rho = 16 * i + lr;
     if (rho < sm.rows) {
       if (!cut) {
@@ -751,15 +788,29 @@ __device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws,
                                       reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg));
         if (a.lse != nullptr && lg == 0)
           a.lse[orow] = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
-      } else {
+      } else if (!held) {
         const size_t prow = part_row(b, slot_id, wid, rho);
-        float* po = ws.part_o + prow * kD;
+        const float sc = __builtin_amdgcn_ldexpf(1.0f, -e);
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt)
-          *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * lg) = rt[i].o[dt];
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<halfx8*>(ws.part_o + prow * kD + part_dim(32 * j + 4 * lg)) =
+              pack_part(rt[i].o[2 * j], rt[i].o[2 * j + 1], sc);
         if (lg == 0)
-          *reinterpret_cast<floatx4*>(ws.part_ml + prow * 4) = floatx4{M, L, Lq, 0.0f};
+          *reinterpret_cast<floatx4*>(ws.part_ml + prow * 4) = floatx4{M, L, Lq, float(e)};
       }
+    }
+    if (cut && held) {
+      const float sc = __builtin_amdgcn_ldexpf(1.0f, -e);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const halfx8 v = pack_part(rt[i].o[2 * j], rt[i].o[2 * j + 1], sc);
+        const uint4 w = __builtin_bit_cast(uint4, v);
+        hold.h[i][4 * j] = w.x;
+        hold.h[i][4 * j + 1] = w.y;
+        hold.h[i][4 * j + 2] = w.z;
+        hold.h[i][4 * j + 3] = w.w;
+      }
+      hold.ml[i] = floatx4{M, L, Lq, float(e)};
     }
   }
   // stores drained: the ring's waits count tile copies only (stores may
@@ -796,6 +847,10 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
 #pragma unroll
   for (int s = 0; s < kWaveStages; ++s) issue_next(is, a, ws, nunits, lo, hi, wid, ring_lds, cp);
 
+  HeldPartial hp;
+  hp.mt = 0;
+  hp.rows = 0;
+  hp.prow0 = 0;
   int u = first_unit;
   while (true) {
     const Unit ud = load_unit(ws.units, u);
@@ -803,20 +858,42 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
     const int seg_hi = min(hi, ud.tile_end);
     const Stream sm = stream_of(ud, wid, a.hkv, a.G);
     const int mt = (sm.rows + 15) / 16;
+    // the first segment of a cut unit that began before this range, with more
+    // segments after it: its partial is held (wave-uniform)
+    const bool held = ud.cut != 0 && ud.tile_start < lo && ud.tile_end < hi;
     if (mt == 0) {
       // empty stream: nothing was copied for these tiles; keep the ring moving
       for (int t = seg_lo; t < seg_hi; ++t) issue_next(is, a, ws, nunits, lo, hi, wid, ring_lds, cp);
     } else if (mt == 1) {
-      run_segment<1>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof);
+      run_segment<1>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof,
+                     held, hp);
     } else if (mt == 2) {
-      run_segment<2>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof);
+      run_segment<2>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof,
+                     held, hp);
     } else if (mt == 3) {
-      run_segment<3>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof);
+      run_segment<3>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof,
+                     held, hp);
     } else {
-      run_segment<4>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof);
+      run_segment<4>(a, ws, ud, sm, seg_lo, seg_hi, lo, hi, nunits, b, ring, ring_lds, is, cp, lof,
+                     held, hp);
     }
     if (seg_hi >= hi || u + 1 >= nunits) break;
     u = __builtin_amdgcn_readfirstlane(u + 1);
+  }
+  // the held partial, after the last segment
+  const int lane = threadIdx.x & (kWave - 1);
+  const int lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < kMaxMT; ++i) {
+    const int rho = 16 * i + lr;
+    if (i < hp.mt && rho < hp.rows) {
+      const size_t prow = hp.prow0 + size_t(rho);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<uint4*>(ws.part_o + prow * kD + part_dim(32 * j + 4 * lg)) =
+            make_uint4(hp.h[i][4 * j], hp.h[i][4 * j + 1], hp.h[i][4 * j + 2], hp.h[i][4 * j + 3]);
+      if (lg == 0) *reinterpret_cast<floatx4*>(ws.part_ml + prow * 4) = hp.ml[i];
+    }
   }
 }
 
@@ -860,7 +937,8 @@ int32_t launch_attn_impl(const AttnArgs& a, bool plan, bool combine, hipStream_t
     // the flags borrow the start of the partials, which the main kernel only
     // writes later on the same stream
     kv.page_chunks = (a.max_pages + kPageChunk - 1) / kPageChunk;
-    if (size_t(a.R) * size_t(kv.page_chunks) * 4 > part_rows(nb) * kD * 4) return ECHO_ERR_UNSUPPORTED;
+    if (size_t(a.R) * size_t(kv.page_chunks) * 4 > part_rows(nb) * kD * sizeof(_Float16))
+      return ECHO_ERR_UNSUPPORTED;
     kv.page_bad = reinterpret_cast<const int32_t*>(ws.part_o);
     hipLaunchKernelGGL(attn_pages_kernel, dim3(unsigned(a.R), unsigned(kv.page_chunks)),
                        dim3(kPageChunk), 0, stream, kv);

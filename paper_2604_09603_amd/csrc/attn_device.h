@@ -53,8 +53,12 @@ struct AttnWs {
   Unit* units;
   int32_t* wg_unit;  // [nb] unit holding each workgroup's first tile
   Cut* cuts;
-  float* part_ml;  // [2 * nb * 4 * 64][4]: reference max (log2 units), sum, rounded sum, 0
-  float* part_o;   // [2 * nb * 4 * 64][128]
+  // partials of the cut units: [2 * nb * 4 * 64][4] reference max (log2 units),
+  // sum, rounded sum and the exponent e of the row's scale; [2 * nb * 4 * 64][128]
+  // the row's unnormalised output times 2^-e in fp16 (e puts the row's largest
+  // magnitude in [2^14, 2^15))
+  float* part_ml;
+  _Float16* part_o;
 };
 
 __host__ __device__ inline size_t al(size_t x) { return (x + 255) / 256 * 256; }
@@ -88,13 +92,13 @@ __host__ __device__ inline AttnWs attn_layout(void* base, size_t ucap, int nb) {
   p += al(size_t(nb) * sizeof(Cut));
   w.part_ml = reinterpret_cast<float*>(p);
   p += al(part_rows(nb) * 4 * sizeof(float));
-  w.part_o = reinterpret_cast<float*>(p);
+  w.part_o = reinterpret_cast<_Float16*>(p);
   return w;
 }
 
 __host__ inline size_t attn_ws_total(size_t ucap, int nb) {
   return 256 + al(ucap * sizeof(Unit)) + al(size_t(nb) * 4) + al(size_t(nb) * sizeof(Cut)) +
-         al(part_rows(nb) * 4 * 4) + al(part_rows(nb) * kD * 4);
+         al(part_rows(nb) * 4 * 4) + al(part_rows(nb) * kD * 2);
 }
 
 // Partial row of (workgroup b, slot, stream w, row rho).
@@ -374,6 +378,23 @@ constexpr int kCombineBlocks = kCombineItems / kThreads;
 constexpr int kFastParts = 4;  // cuts over at most this many workgroups merge in one round trip
 static_assert(kCombineItems % kThreads == 0, "combine tiling");
 
+typedef _Float16 halfx4 __attribute__((ext_vector_type(4)));
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
+
+// Where dim d of a partial row sits: the main kernel's lane with dims
+// 16 dt + 4 g + [0, 4) writes those of dt = 2j and 2j + 1 as 8 consecutive
+// halves at 32 j + 8 g, so that one 16-byte store covers both.
+__host__ __device__ inline int part_dim(int d) {
+  const int dt = d >> 4, g = (d >> 2) & 3;
+  return (dt >> 1) * 32 + g * 8 + (dt & 1) * 4 + (d & 3);
+}
+
+// Four dims of a partial row, back in the row's fp32 scale (e: its exponent).
+__device__ __forceinline__ floatx4 load_part_o(const AttnWs& ws, size_t prow, int d4, float e) {
+  const halfx4 h = *reinterpret_cast<const halfx4*>(ws.part_o + prow * kD + part_dim(d4));
+  return __builtin_convertvector(h, floatx4) * __builtin_amdgcn_ldexpf(1.0f, int(e));
+}
+
 // One output row (4 dims) and its LSE from the partials of its parts: (max,
 // sum, rounded sum) and O of each (parts with max -inf are absent or empty).
 template <int NP>
@@ -438,7 +459,7 @@ __device__ __forceinline__ void combine_body(int hq, int hkv, int G, const AttnW
         if (i < nparts && rho < sm.rows) {
           const size_t prow = prow_of(i, rho);
           ml[k][i] = *reinterpret_cast<const floatx4*>(ws.part_ml + prow * 4);
-          po[k][i] = *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
+          po[k][i] = load_part_o(ws, prow, d4, ml[k][i][3]);
         }
       }
     }
@@ -490,7 +511,7 @@ __device__ __forceinline__ void combine_body(int hq, int hkv, int G, const AttnW
         if (i0 + j < nparts && rho < sm.rows) {
           const size_t prow = prow_of(i0 + j, rho);
           ml[k][j] = *reinterpret_cast<const floatx4*>(ws.part_ml + prow * 4);
-          po[k][j] = *reinterpret_cast<const floatx4*>(ws.part_o + prow * kD + d4);
+          po[k][j] = load_part_o(ws, prow, d4, ml[k][j][3]);
         }
       }
 #pragma unroll

@@ -231,8 +231,11 @@ def test_late_dominant_key_every_row(seed):
     reference, so the late key's probability is 2^(1 + e), not a power of two,
     and its bf16 rounding moves the output by up to 2^-9 of the value spread
     (6e-3 to 9e-3 on these batches) unless the residual product runs (3e-4).
-    The kernel screens that test with a threshold taken at earlier tiles; the
-    bound of 1.5e-3 on every row shows the late tile still got through."""
+    Rows of units cut between workgroups are merged from partials stored in
+    fp16, each row scaled by a power of two: their rounding is 2^-12 of the
+    row's largest value, up to 2e-3 here (values of V times 4).  The kernel
+    screens the residual test with a threshold taken at earlier tiles; the bound
+    of 3e-3 on every row shows the late tile still got through."""
     rng = np.random.default_rng(500 + seed)
     R, hq, hkv = 8, 32, 2
     G = hq // hkv
@@ -272,7 +275,7 @@ def test_late_dominant_key_every_row(seed):
     err = np.abs(res["out"][:nq].astype(np.float64) - ro[:nq]).max()
     print(f"[edges] late dominant key, seed {seed}: max abs {err:.2e} over {nq * hq} rows",
           flush=True)
-    assert err <= 1.5e-3, f"max abs error {err:.3e}: the late tile's residual product did not run"
+    assert err <= 3e-3, f"max abs error {err:.3e}: the late tile's residual product did not run"
 
 
 def test_empty_requests_and_prefixes():
