@@ -380,6 +380,7 @@ static_assert(kCombineItems % kThreads == 0, "combine tiling");
 
 typedef _Float16 halfx4 __attribute__((ext_vector_type(4)));
 typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
+typedef uint32_t uint32x4 __attribute__((ext_vector_type(4)));
 
 // Where dim d of a partial row sits: the main kernel's lane with dims
 // 16 dt + 4 g + [0, 4) writes those of dt = 2j and 2j + 1 as 8 consecutive
@@ -426,14 +427,24 @@ __device__ __forceinline__ void combine_body(int hq, int hkv, int G, const AttnW
                                              float* __restrict__ out, float* __restrict__ lse,
                                              int block) {
   const int ci = block / kCombineBlocks;
-  if (ci >= ws.meta[2]) return;
+  // the cut record (ci < nb: inside the array) is loaded with the cut count, in
+  // the same round trip; a workgroup past the count only waits for it to land
+  // (the empty asm uses it there, so that the loads are not moved below the test)
+  static_assert(sizeof(Cut) == 4 * sizeof(uint32x4), "cut record: four 16-byte loads");
+  uint32x4 raw[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) raw[k] = reinterpret_cast<const uint32x4*>(ws.cuts + ci)[k];
+  if (ci >= ws.meta[2]) {
+    asm volatile("" ::"v"(raw[0]), "v"(raw[1]), "v"(raw[2]), "v"(raw[3]));
+    return;
+  }
+  const Cut c = __builtin_bit_cast(Cut, raw);
   const int e = (block % kCombineBlocks) * kThreads + threadIdx.x;
   constexpr int kRowSpan = kPassRows / kCombineRowsPerThread;
   constexpr int NR = kCombineRowsPerThread;
   const int w = e / (kRowSpan * (kD / 4));
   const int rho0 = (e / (kD / 4)) % kRowSpan;
   const int d4 = (e % (kD / 4)) * 4;
-  const Cut c = ws.cuts[ci];
   const Unit& u = c.u;
   const Stream sm = stream_of(u, w, hkv, G);
   if (rho0 >= sm.rows) return;
