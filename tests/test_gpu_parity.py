@@ -115,3 +115,27 @@ def test_repeat_is_bit_identical():
     second = st.fetch()
     for k in ["out", "lse", "selected", "tree_mask", "accept_len", "path_score"]:
         assert np.array_equal(np.asarray(first[k]).view(np.uint8), np.asarray(second[k]).view(np.uint8)), k
+
+
+@pytest.mark.parametrize("name", ["l8b", "q235b"])
+def test_large_values_through_cut_units(name):
+    """Values scaled by 2^14 (outputs of order 10^4, far past the fp16 range once
+    summed over a workgroup's keys): the partials of units cut between
+    workgroups are stored in fp16 with a power-of-two scale per row, so the
+    merged rows stay finite and within the row-relative bound, like the rows
+    written directly.  Every slot of 8 requests plus 256 random slots."""
+    b = synth.make_batch(name, 13, v_scale=float(2 ** 14))
+    ref = gc.oracle_front(b)
+    st, res = gc.run_gpu(b, ref["target"])
+    gc.compare_front(res, ref, int(b["cand_offsets"][-1]))
+    m = ref["mask"]
+    rows = gc.sample_rows(m["q_offsets"], np.random.default_rng(6), n_requests=8, n_extra=256)
+    ro, rl = _attn_ref(b, m, rows)
+    ro, rl = ro[rows], rl[rows]
+    o = res["out"][rows].astype(np.float64)
+    assert np.isfinite(o).all(), "non-finite output rows"
+    scale = np.maximum(np.abs(ro).max(axis=-1), 1e-6)
+    rel = (np.abs(o - ro).max(axis=-1) / scale).max()
+    _log(f"[parity] {name} V x2^14: row rel {rel:.2e}, largest output {np.abs(ro).max():.3e}")
+    assert rel <= gc.RTOL_ROW, f"row-relative error {rel:.3e}"
+    assert np.abs(res["lse"][rows] - rl).max() <= gc.LSE_ATOL
