@@ -61,7 +61,8 @@ __global__ __launch_bounds__(kPageChunk) void attn_pages_kernel(KvSource kv) {
 __global__ __launch_bounds__(kThreads) void attn_plan_kernel(
     const int32_t* __restrict__ q_offsets, KvSource kv, int R, int hkv, int G, int max_rows,
     int nb, long long ucap, AttnWs ws, int32_t* status) {
-  plan_body<kThreads>(q_offsets, kv, R, hkv, G, max_rows, nb, ucap, ws, status);
+  extern __shared__ int32_t plan_tables[];  // plan_table_words(min(R, kThreads))
+  plan_body<kThreads>(q_offsets, kv, R, hkv, G, max_rows, nb, ucap, ws, status, plan_tables);
 }
 
 // ---------------------------------------------------------------- main ----
@@ -539,6 +540,16 @@ __device__ __forceinline__ Unit load_unit(const Unit* units, int i) {
   return u;
 }
 
+// A workgroup's start record, through the constant address space as the units.
+__device__ __forceinline__ WgStart load_wg_start(const WgStart* starts, int b) {
+  static_assert(sizeof(WgStart) == 16 * sizeof(int32_t), "start record layout");
+  const_i32_t* p = (const_i32_t*)(starts + b);
+  int32_t w[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) w[k] = p[k];
+  return __builtin_bit_cast(WgStart, w);
+}
+
 // Issue side of a wave's ring: the wave's k-th tile is lo + k; its copy goes to
 // stage k % 2 (nothing is copied where the wave's stream of the unit is empty).
 struct Issuer {
@@ -821,11 +832,10 @@ __device__ __forceinline__ void run_segment(const MainArgs& a, const AttnWs& ws,
 __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a, AttnWs ws) {
   __shared__ __attribute__((aligned(1024))) char smem[kMainLds];
   const int b = blockIdx.x;
-  const int nw = ws.meta[3];
-  if (b >= nw) return;
-  const long long T = ws.meta[1];
-  const int lo = int(range_lo(T, b, nw));
-  const int hi = int(range_lo(T, b + 1, nw));
+  // one round trip before the first copy: the range, the unit count and the
+  // first unit come in one record
+  const WgStart st = load_wg_start(ws.wg_start, b);
+  const int lo = st.lo, hi = st.hi;
   const int wid = wave_id();
   const CopyPlan cp = copy_plan(uint32_t(a.hkv) * kD * 2);
   const LaneOffsets lof = lane_offsets();
@@ -833,15 +843,17 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
   // the ring's LDS address (wave-uniform), for the copies
   const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(
       uint32_t(reinterpret_cast<uintptr_t>((lds_void_t*)ring)));
-  const int nunits = ws.meta[0];
+  const int nunits = st.nunits;
 
   // the wave walks the units from the one holding the range's first tile; the
   // issue side runs ahead of it
-  const int first_unit = __builtin_amdgcn_readfirstlane(ws.wg_unit[b]);
+  const int first_unit = st.first_unit;
   Issuer is;
   is.iu = first_unit;
-  is.ud = load_unit(ws.units, is.iu);
+  is.ud = st.u;
   issuer_unit(is, a, wid);
+  // (after the set-up, so that its loads are issued with the record's)
+  if (lo >= hi) return;
   is.k = 0;
   is.copied = 0u;
 #pragma unroll
@@ -852,8 +864,8 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
   hp.rows = 0;
   hp.prow0 = 0;
   int u = first_unit;
+  Unit ud = st.u;
   while (true) {
-    const Unit ud = load_unit(ws.units, u);
     const int seg_lo = max(lo, ud.tile_start);
     const int seg_hi = min(hi, ud.tile_end);
     const Stream sm = stream_of(ud, wid, a.hkv, a.G);
@@ -879,6 +891,7 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
     }
     if (seg_hi >= hi || u + 1 >= nunits) break;
     u = __builtin_amdgcn_readfirstlane(u + 1);
+    ud = load_unit(ws.units, u);
   }
   // the held partial, after the last segment
   const int lane = threadIdx.x & (kWave - 1);
@@ -944,8 +957,10 @@ int32_t launch_attn_impl(const AttnArgs& a, bool plan, bool combine, hipStream_t
                        dim3(kPageChunk), 0, stream, kv);
   }
   if (plan)
-    hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kThreads), 0, stream, a.q_offsets, kv, a.R,
-                       a.hkv, G, a.max_rows, nb, static_cast<long long>(ucap), ws, a.status);
+    hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(kThreads),
+                       plan_table_words(a.R < kThreads ? a.R : kThreads) * sizeof(int32_t), stream,
+                       a.q_offsets, kv, a.R, a.hkv, G, a.max_rows, nb,
+                       static_cast<long long>(ucap), ws, a.status);
   MainArgs m;
   m.q = a.q;
   m.k_new = a.k_new;

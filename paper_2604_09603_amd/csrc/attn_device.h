@@ -48,10 +48,18 @@ struct Cut {
   Unit u;                            // the unit itself (the merge needs no second lookup)
 };
 
+// What a workgroup of the main kernel needs before its first copy, in one
+// 64-byte record: its tile range [lo, hi) (lo == hi: no work), the number of
+// units, the unit holding tile lo and a copy of that unit.
+struct WgStart {
+  int32_t lo, hi, nunits, first_unit;
+  Unit u;
+};
+
 struct AttnWs {
   int32_t* meta;   // [0] units, [1] tiles, [2] cut units, [3] workgroups with work
   Unit* units;
-  int32_t* wg_unit;  // [nb] unit holding each workgroup's first tile
+  WgStart* wg_start;  // [nb], written for every workgroup by each plan
   Cut* cuts;
   // partials of the cut units: [2 * nb * 4 * 64][4] reference max (log2 units),
   // sum, rounded sum and the exponent e of the row's scale; [2 * nb * 4 * 64][128]
@@ -86,8 +94,8 @@ __host__ __device__ inline AttnWs attn_layout(void* base, size_t ucap, int nb) {
   p += 256;
   w.units = reinterpret_cast<Unit*>(p);
   p += al(ucap * sizeof(Unit));
-  w.wg_unit = reinterpret_cast<int32_t*>(p);
-  p += al(size_t(nb) * sizeof(int32_t));
+  w.wg_start = reinterpret_cast<WgStart*>(p);
+  p += al(size_t(nb) * sizeof(WgStart));
   w.cuts = reinterpret_cast<Cut*>(p);
   p += al(size_t(nb) * sizeof(Cut));
   w.part_ml = reinterpret_cast<float*>(p);
@@ -97,7 +105,8 @@ __host__ __device__ inline AttnWs attn_layout(void* base, size_t ucap, int nb) {
 }
 
 __host__ inline size_t attn_ws_total(size_t ucap, int nb) {
-  return 256 + al(ucap * sizeof(Unit)) + al(size_t(nb) * 4) + al(size_t(nb) * sizeof(Cut)) +
+  return 256 + al(ucap * sizeof(Unit)) + al(size_t(nb) * sizeof(WgStart)) +
+         al(size_t(nb) * sizeof(Cut)) +
          al(part_rows(nb) * 4 * 4) + al(part_rows(nb) * kD * 2);
 }
 
@@ -236,13 +245,48 @@ __device__ __forceinline__ RequestShape request_shape_at(const int32_t* q_offset
   return request_shape(load_request(q_offsets, kv, r), kv, ok, R, hkv, G, r);
 }
 
+// Unit g of a request of shape s whose tiles start at tile tb; b0 and b1: the
+// workgroups whose ranges hold its first and its last tile.
+__device__ __forceinline__ Unit make_unit(const RequestShape& s, int tb, int g, long long T, int nw,
+                                          const DivBy& by_t, int& b0, int& b1) {
+  Unit u;
+  u.tile_start = tb + g * s.tiles;
+  u.tile_end = u.tile_start + s.tiles;
+  u.q0 = s.q0;
+  u.nslots = s.nsl;
+  u.kb = s.kb;
+  u.P = s.P;
+  u.ntail = s.ntail;
+  u.passes = s.passes;
+  u.rpp = s.rpp;
+  u.group = g;
+  b0 = range_of(u.tile_start, T, nw, by_t);
+  b1 = range_of(u.tile_end - 1, T, nw, by_t);
+  u.cut = b0 != b1;
+  u.pad = 0;
+  return u;
+}
+
+// LDS (32-bit words) for the plan's request tables when it runs with one
+// request per thread: tile and unit bases and the shapes of R requests.
+__host__ __device__ inline size_t plan_table_words(int R) {
+  return size_t(2) * (R + 1) + size_t(R) * (sizeof(RequestShape) / 4);
+}
+
 // The plan on one workgroup of NT threads (see attn_plan above): the units,
-// each workgroup's first unit and the cut units, written to ws; meta[0..3] =
+// each workgroup's start record and the cut units, written to ws; meta[0..3] =
 // units, tiles, cut units, workgroups with work.
+// * `tables` (may be null): plan_table_words(min(R, NT)) words of LDS.  With it
+//   and R <= NT, one thread per workgroup writes the start records, from the
+//   request tables; without it, the thread of the request holding a range's
+//   first tile writes that range's record.
+// * `pre` (may be null): request threadIdx.x's fields as load_request gives
+//   them, already in hand (R <= NT).
 template <int NT>
 __device__ void plan_body(const int32_t* __restrict__ q_offsets, const KvSource& kv, int R, int hkv,
                           int G, int max_rows, int nb, long long ucap, const AttnWs& ws,
-                          int32_t* status) {
+                          int32_t* status, int32_t* tables = nullptr,
+                          const RequestIn* pre = nullptr) {
   __shared__ int s_scan[NT / kWave + 1];
   __shared__ int2 s_scan2[NT / kWave + 1];
   __shared__ uint8_t s_ok[ECHO_MAX_REQUESTS + 1];
@@ -255,7 +299,7 @@ __device__ void plan_body(const int32_t* __restrict__ q_offsets, const KvSource&
   int ub1 = 0, tb1 = 0;
   int bits = 0;
   for (int r = tid; r < R; r += NT) {
-    const RequestIn in = load_request(q_offsets, kv, r);
+    const RequestIn in = single && pre != nullptr ? *pre : load_request(q_offsets, kv, r);
     bool ok = request_ok(in, kv, max_rows);
     if (kv.block_table != nullptr)
       for (int c = 0; c < kv.page_chunks; ++c) ok = ok && kv.page_bad[size_t(r) * kv.page_chunks + c] == 0;
@@ -284,7 +328,12 @@ __device__ void plan_body(const int32_t* __restrict__ q_offsets, const KvSource&
   }
   // slot ranges that overlap (a non-monotone CSR) could ask for more units than
   // the workspace holds, and tile indices are 32-bit: then nothing is scheduled
-  if (U > ucap || T > 0x7FFFFFFFll) {
+  // workgroups with work: never more than tiles, so that no range is empty
+  const bool fits = U <= ucap && T <= 0x7FFFFFFFll;
+  const int nw = !fits ? 0 : T < nb ? int(T) : nb;
+  // the workgroups without work get an empty range
+  for (int b = nw + tid; b < nb; b += NT) ws.wg_start[b] = WgStart{};
+  if (!fits) {
     if (tid == 0) {
       bits |= ECHO_DATA_BAD_OFFSETS;
       ws.meta[0] = 0;
@@ -296,10 +345,12 @@ __device__ void plan_body(const int32_t* __restrict__ q_offsets, const KvSource&
     return;
   }
   wave_status_or(status, bits);
-  // workgroups with work: never more than tiles, so that no range is empty
-  const int nw = T < nb ? int(T) : nb;
-  // pass B: units, the cut units and each workgroup's first unit
+  // pass B: units, the cut units and each workgroup's start record
   const DivBy by_t(T > 0 ? T : 1), by_nw(nw > 0 ? nw : 1);
+  const bool by_wg = single && tables != nullptr;
+  int32_t* s_tb = tables;             // R + 1: first tile of each request's units, then T
+  int32_t* s_ub = tables + (R + 1);   // R: first unit of each request
+  RequestShape* s_sh = reinterpret_cast<RequestShape*>(tables + 2 * (R + 1));  // R
   int unit_run = 0, tile_run = 0, cut_run = 0;
   for (int base = 0; base < R; base += NT) {
     RequestShape s;
@@ -325,22 +376,16 @@ __device__ void plan_body(const int32_t* __restrict__ q_offsets, const KvSource&
     }
     int tot_c;
     const int cb = cut_run + block_exclusive_sum<NT>(ncut, s_scan, &tot_c);
+    if (by_wg && tid < R) {
+      s_tb[tid] = tb;
+      s_ub[tid] = ub;
+      s_sh[tid] = s;
+    }
+    if (by_wg && tid == 0) s_tb[R] = int(T);
     int c = cb;
     for (int g = 0; g < s.groups; ++g) {
-      Unit u;
-      u.tile_start = tb + g * s.tiles;
-      u.tile_end = u.tile_start + s.tiles;
-      u.q0 = s.q0;
-      u.nslots = s.nsl;
-      u.kb = s.kb;
-      u.P = s.P;
-      u.ntail = s.ntail;
-      u.passes = s.passes;
-      u.rpp = s.rpp;
-      u.group = g;
-      const int b0 = range_of(u.tile_start, T, nw, by_t), b1 = range_of(u.tile_end - 1, T, nw, by_t);
-      u.cut = b0 != b1;
-      u.pad = 0;
+      int b0, b1;
+      const Unit u = make_unit(s, tb, g, T, nw, by_t, b0, b1);
       ws.units[ub + g] = u;
       if (u.cut) {
         Cut cu;
@@ -351,14 +396,49 @@ __device__ void plan_body(const int32_t* __restrict__ q_offsets, const KvSource&
         cu.u = u;
         ws.cuts[c++] = cu;
       }
+      if (by_wg) continue;
       // workgroups whose range starts inside this unit
       int b = b0;
-      if (range_lo(T, b, by_nw) < u.tile_start) ++b;
-      for (; b <= b1; ++b) ws.wg_unit[b] = ub + g;
+      long long blo = range_lo(T, b, by_nw);
+      if (blo < u.tile_start) {
+        ++b;
+        blo = range_lo(T, b, by_nw);
+      }
+      for (; b <= b1; ++b) {
+        const long long bhi = range_lo(T, b + 1, by_nw);
+        WgStart st;
+        st.lo = int(blo);
+        st.hi = int(bhi);
+        st.nunits = int(U);
+        st.first_unit = ub + g;
+        st.u = u;
+        ws.wg_start[b] = st;
+        blo = bhi;
+      }
     }
     unit_run += tot_u;
     tile_run += tot_t;
     cut_run += tot_c;
+  }
+  if (by_wg) {
+    // one workgroup per thread: the request holding the range's first tile is
+    // the last one whose units start at or before it (requests without tiles
+    // share their successor's start)
+    __syncthreads();
+    for (int b = tid; b < nw; b += NT) {
+      const int blo = int(range_lo(T, b, by_nw));
+      const int r = upper_bound_idx(s_tb, R + 1, blo);
+      const RequestShape s = s_sh[r];
+      const int g = s.tiles > 0 ? (blo - s_tb[r]) / s.tiles : 0;
+      int b0, b1;
+      WgStart st;
+      st.lo = blo;
+      st.hi = int(range_lo(T, b + 1, by_nw));
+      st.nunits = int(U);
+      st.first_unit = s_ub[r] + g;
+      st.u = make_unit(s, s_tb[r], g, T, nw, by_t, b0, b1);
+      ws.wg_start[b] = st;
+    }
   }
   if (tid == 0) {
     ws.meta[0] = unit_run;

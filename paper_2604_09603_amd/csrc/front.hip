@@ -60,6 +60,15 @@ __global__ __launch_bounds__(kFrontThreads) void front_kernel(FrontArgs a) {
   // The request tables of flatten & pack are loaded first, into registers, so
   // that their memory latency passes with that of the gate's first loads.
   const MaskTables tab = load_mask_tables(a.cand_offsets, a.root_token, a.prefix_len, a.R);
+  // and the plan's KV offsets (one request per thread), which no phase before
+  // it writes
+  const int tid = threadIdx.x;
+  const bool pre = a.plan && a.R <= kFrontThreads;
+  long long k0 = 0, k1 = 0;
+  if (pre && tid < a.R) {
+    k0 = a.kv.kv_offsets[tid];
+    k1 = a.kv.kv_offsets[tid + 1];
+  }
   if (a.N > 0)  // as the gate call, which skips its last phase without candidates
     gate_finish_body(a.N, a.nblocks, a.gws, a.selected, a.status,
                      FinishLds{reinterpret_cast<uint32_t*>(smem), smem + kSortCap,
@@ -70,15 +79,27 @@ __global__ __launch_bounds__(kFrontThreads) void front_kernel(FrontArgs a) {
                       a.status, smem);
   if (!a.plan) return;
   __syncthreads();
+  // the slot offsets the mask phase just wrote are still in its LDS table
+  const int32_t* s_qoff = smem + (a.R + 1);
+  RequestIn in;
+  in.q0 = tid < a.R ? s_qoff[tid] : 0;
+  in.q1 = tid < a.R ? s_qoff[tid + 1] : 0;
+  in.k0 = k0;
+  in.k1 = k1;
+  in.P = k1 - k0;
+  // (the tables reuse the LDS of the phases before; every thread has read its
+  // slot offsets before the plan's first barrier)
   plan_body<kFrontThreads>(a.q_offsets, a.kv, a.R, a.hkv, a.G, a.max_rows, a.nb, a.ucap, a.aws,
-                           a.status);
+                           a.status, smem, pre ? &in : nullptr);
 }
 
 }  // namespace
 
 size_t front_lds_bytes(int32_t R, int32_t budget) {
   const size_t m = mask_lds_bytes(R, budget);
-  return m > kFinishLds ? m : kFinishLds;
+  const size_t p = plan_table_words(R < kFrontThreads ? R : kFrontThreads) * sizeof(int32_t);
+  const size_t f = m > kFinishLds ? m : kFinishLds;
+  return f > p ? f : p;
 }
 
 int32_t launch_front(const FrontLaunch& f, hipStream_t stream) {
