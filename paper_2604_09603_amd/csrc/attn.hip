@@ -911,10 +911,11 @@ __global__ __launch_bounds__(kWaves * kWave, 1) void attn_main_kernel(MainArgs a
 }
 
 // ------------------------------------------------------------- combine ----
+template <int NR>
 __global__ __launch_bounds__(kThreads) void attn_combine_kernel(int hq, int hkv, int G, AttnWs ws,
                                                                 float* __restrict__ out,
                                                                 float* __restrict__ lse) {
-  combine_body(hq, hkv, G, ws, out, lse, blockIdx.x);
+  combine_body<NR>(hq, hkv, G, ws, out, lse, blockIdx.x);
 }
 
 int main_workgroups() { return device_cu_count(); }
@@ -989,9 +990,17 @@ int32_t launch_attn_impl(const AttnArgs& a, bool plan, bool combine, hipStream_t
                          0) != hipSuccess)
     return ECHO_ERR_HIP;
   // cut units number fewer than the main kernel's workgroups
-  if (combine)
-    hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(nb * kCombineBlocks)), dim3(kThreads), 0,
-                       stream, a.hq, a.hkv, G, ws, a.out, a.lse);
+  if (combine) {
+    const long long cache_rows = a.block_table == nullptr
+                                     ? static_cast<long long>(a.kv_rows)
+                                     : static_cast<long long>(a.num_pages) * a.page_size;
+    if (combine_rows_per_thread(a.R, a.max_rows, a.hq, a.hkv, nb, cache_rows) == 1)
+      hipLaunchKernelGGL(attn_combine_kernel<1>, dim3(unsigned(nb * combine_blocks<1>())),
+                         dim3(kThreads), 0, stream, a.hq, a.hkv, G, ws, a.out, a.lse);
+    else
+      hipLaunchKernelGGL(attn_combine_kernel<2>, dim3(unsigned(nb * combine_blocks<2>())),
+                         dim3(kThreads), 0, stream, a.hq, a.hkv, G, ws, a.out, a.lse);
+  }
   return hipGetLastError() == hipSuccess ? ECHO_OK : ECHO_ERR_HIP;
 }
 

@@ -449,14 +449,37 @@ __device__ void plan_body(const int32_t* __restrict__ q_offsets, const KvSource&
 }
 
 // ------------------------------------------------------------- combine ----
-// One thread per (cut unit, stream, pair of rows, 4 dims): rows rho and
-// rho + 32 of the stream; a cut's items span kCombineBlocks workgroups.  The
+// One thread per (cut unit, stream, NR rows, 4 dims): rows rho, rho + 64 / NR, ...
+// of the stream; a cut's items span combine_blocks<NR>() workgroups.  The
 // partials are merged in workgroup order.
-constexpr int kCombineRowsPerThread = 2;
-constexpr int kCombineItems = kWaves * (kPassRows / kCombineRowsPerThread) * (kD / 4);
-constexpr int kCombineBlocks = kCombineItems / kThreads;
+template <int NR>
+constexpr int combine_blocks() {
+  static_assert((kWaves * (kPassRows / NR) * (kD / 4)) % kThreads == 0, "combine tiling");
+  return kWaves * (kPassRows / NR) * (kD / 4) / kThreads;
+}
 constexpr int kFastParts = 4;  // cuts over at most this many workgroups merge in one round trip
-static_assert(kCombineItems % kThreads == 0, "combine tiling");
+
+// Rows per combine thread for a launch.  Two rows per thread load both rows'
+// partials in one round trip with half the threads; one row per thread needs
+// half the registers, so more waves wait at once.  The second wins when cuts
+// span many workgroups (their rows merge in several batches): with U units over
+// nb workgroups a cut spans about 1 + nb / U of them.  U is estimated from the
+// mean slots per request (max_rows / R), as the plan shapes requests.  With
+// fewer tiles than about two per workgroup (kv_rows: the cache's rows, an upper
+// bound of the prefixes) most of the grid has no cut to merge, and the smaller
+// grid of two rows per thread is kept.
+__host__ inline int combine_rows_per_thread(int R, int max_rows, int hq, int hkv, int nb,
+                                            long long kv_rows) {
+  if (R <= 0 || hkv <= 0) return 2;
+  const int rows = (max_rows / R) * (hq / hkv);
+  int passes = (rows + kPassRows - 1) / kPassRows;
+  passes = passes > 0 ? passes : 1;
+  const int fill = fill_passes(hkv) < rows ? fill_passes(hkv) : rows;
+  passes = passes > fill ? passes : fill;
+  const long long units = (long long)R * ((hkv * passes + kWaves - 1) / kWaves);
+  const long long tiles = units * ((kv_rows / R + kTileKeys - 1) / kTileKeys + 1);
+  return units * 3 <= nb && tiles >= 2LL * nb ? 1 : 2;
+}
 
 typedef _Float16 halfx4 __attribute__((ext_vector_type(4)));
 typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
@@ -476,6 +499,13 @@ __device__ __forceinline__ floatx4 load_part_o(const AttnWs& ws, size_t prow, in
   return __builtin_convertvector(h, floatx4) * __builtin_amdgcn_ldexpf(1.0f, int(e));
 }
 
+// acc + w * v, fused in every lane: the merges round the same way whatever the
+// code around them (the combine's launch shapes give bit-identical rows).
+__device__ __forceinline__ floatx4 fma4(float w, const floatx4& v, const floatx4& acc) {
+  return floatx4{__builtin_fmaf(w, v[0], acc[0]), __builtin_fmaf(w, v[1], acc[1]),
+                 __builtin_fmaf(w, v[2], acc[2]), __builtin_fmaf(w, v[3], acc[3])};
+}
+
 // One output row (4 dims) and its LSE from the partials of its parts: (max,
 // sum, rounded sum) and O of each (parts with max -inf are absent or empty).
 template <int NP>
@@ -492,9 +522,9 @@ __device__ __forceinline__ void merge_parts(const floatx4 (&ml)[NP], const float
     for (int i = 0; i < NP; ++i) {
       if (i >= np || ml[i][0] == -__builtin_inff()) continue;
       const float wgt = __builtin_amdgcn_exp2f(ml[i][0] - M);
-      L += wgt * ml[i][1];
-      Lq += wgt * ml[i][2];
-      acc += wgt * po[i];
+      L = __builtin_fmaf(wgt, ml[i][1], L);
+      Lq = __builtin_fmaf(wgt, ml[i][2], Lq);
+      acc = fma4(wgt, po[i], acc);
     }
   }
   const float inv = Lq > 0.0f ? 1.0f / Lq : 0.0f;
@@ -502,11 +532,14 @@ __device__ __forceinline__ void merge_parts(const floatx4 (&ml)[NP], const float
   if (l != nullptr) *l = L > 0.0f ? (M + log2f(L)) * kLn2 : -__builtin_inff();
 }
 
-// Workgroup `block` of the combine (kThreads threads; kCombineBlocks per cut unit).
+// Workgroup `block` of the combine (kThreads threads; combine_blocks<NR>() per
+// cut unit).
+template <int NR>
 __device__ __forceinline__ void combine_body(int hq, int hkv, int G, const AttnWs& ws,
                                              float* __restrict__ out, float* __restrict__ lse,
                                              int block) {
-  const int ci = block / kCombineBlocks;
+  constexpr int kBlocks = combine_blocks<NR>();
+  const int ci = block / kBlocks;
   // the cut record (ci < nb: inside the array) is loaded with the cut count, in
   // the same round trip; a workgroup past the count only waits for it to land
   // (the empty asm uses it there, so that the loads are not moved below the test)
@@ -519,9 +552,8 @@ __device__ __forceinline__ void combine_body(int hq, int hkv, int G, const AttnW
     return;
   }
   const Cut c = __builtin_bit_cast(Cut, raw);
-  const int e = (block % kCombineBlocks) * kThreads + threadIdx.x;
-  constexpr int kRowSpan = kPassRows / kCombineRowsPerThread;
-  constexpr int NR = kCombineRowsPerThread;
+  const int e = (block % kBlocks) * kThreads + threadIdx.x;
+  constexpr int kRowSpan = kPassRows / NR;
   const int w = e / (kRowSpan * (kD / 4));
   const int rho0 = (e / (kD / 4)) % kRowSpan;
   const int d4 = (e % (kD / 4)) * 4;
@@ -612,9 +644,9 @@ __device__ __forceinline__ void combine_body(int hq, int hkv, int G, const AttnW
       for (int j = 0; j < kFastParts; ++j) {
         if (ml[k][j][0] == -__builtin_inff()) continue;
         const float wgt = __builtin_amdgcn_exp2f(ml[k][j][0] - M[k]);
-        L[k] += wgt * ml[k][j][1];
-        Lq[k] += wgt * ml[k][j][2];
-        acc[k] += wgt * po[k][j];
+        L[k] = __builtin_fmaf(wgt, ml[k][j][1], L[k]);
+        Lq[k] = __builtin_fmaf(wgt, ml[k][j][2], Lq[k]);
+        acc[k] = fma4(wgt, po[k][j], acc[k]);
       }
     }
   }

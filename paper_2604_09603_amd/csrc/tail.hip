@@ -35,6 +35,7 @@ struct TailArgs {
   int32_t* status;
 };
 
+template <int NR>
 __global__ __launch_bounds__(kThreads) void tail_kernel(TailArgs a) {
   __shared__ int32_t s_stage[kAcceptWaves][3][kTailStage];
   const int b = blockIdx.x;
@@ -47,7 +48,7 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(TailArgs a) {
                      AcceptLds{s_stage[w][0], s_stage[w][1], s_stage[w][2], kTailStage});
     return;
   }
-  combine_body(a.hq, a.hkv, a.G, a.ws, a.out, a.lse, b - a.nacc);
+  combine_body<NR>(a.hq, a.hkv, a.G, a.ws, a.out, a.lse, b - a.nacc);
 }
 
 }  // namespace
@@ -76,8 +77,15 @@ int32_t launch_tail(const AttnArgs& a, const int32_t* slot_parent, const int32_t
   t.accept_slots = accept_slots;
   t.bonus_token = bonus_token;
   t.status = a.status;
-  hipLaunchKernelGGL(tail_kernel, dim3(unsigned(t.nacc + nb * kCombineBlocks)), dim3(kThreads), 0,
-                     stream, t);
+  const long long cache_rows = a.block_table == nullptr
+                                   ? static_cast<long long>(a.kv_rows)
+                                   : static_cast<long long>(a.num_pages) * a.page_size;
+  if (combine_rows_per_thread(a.R, a.max_rows, a.hq, a.hkv, nb, cache_rows) == 1)
+    hipLaunchKernelGGL(tail_kernel<1>, dim3(unsigned(t.nacc + nb * combine_blocks<1>())),
+                       dim3(kThreads), 0, stream, t);
+  else
+    hipLaunchKernelGGL(tail_kernel<2>, dim3(unsigned(t.nacc + nb * combine_blocks<2>())),
+                       dim3(kThreads), 0, stream, t);
   return hipGetLastError() == hipSuccess ? ECHO_OK : ECHO_ERR_HIP;
 }
 
