@@ -375,28 +375,27 @@ __global__ __launch_bounds__(kGateThreads) void gate_select_kernel(int N, int nb
                                                                    int32_t* status) {
   __shared__ uint32_t s_cnt;
   const int g = blockIdx.x * kGateThreads + threadIdx.x;
-  // this thread's key and parent are fetched while the bin is found
+  // this thread's key is fetched while the bin is found
   const uint32_t k = g < N ? ws.keys[g] : 0u;
-  const int32_t p = g < N ? ws.pglob[g] : -1;
   if (threadIdx.x == 0) s_cnt = 0u;
   const BinResult br = find_bin(nblocks, budget, ws, blockIdx.x == 0, num_selected);
   const uint32_t m = br.m;
   const uint32_t bin = br.bin;
-  int bits = 0;
   if (g < N) {
     const uint32_t kb = k >> kHistShift;
     if (m == 0u || k == 0u || kb < bin) {
       selected[g] = 0;
     } else if (kb > bin) {
+      // selected, and so is its parent: the child's score is the parent's plus a
+      // clamped log q <= 0 in one binary32 add, so the parent's key (same walk,
+      // same clamps) is never below the child's and lies in a higher bin too
       selected[g] = 1;
-      // a parent's key is never below its child's, so it lies in a higher bin too
-      if (p >= 0 && !(ws.keys[p] >> kHistShift > bin)) bits |= ECHO_DATA_NOT_CLOSED;
     } else {
       const uint32_t slot = atomicAdd(&s_cnt, 1u);  // LDS; the order is fixed by the finish
       ws.cand[size_t(blockIdx.x) * kGateThreads + slot] = make_uint2(k, uint32_t(g));
     }
   }
-  wave_status_or(status, bits);
+  (void)status;  // nothing above the threshold bin can be unclosed (see above)
   __syncthreads();
   if (threadIdx.x == 0) ws.ccount[blockIdx.x] = s_cnt;
 }
