@@ -228,12 +228,11 @@ __device__ void gate_finish_body(int N, int nblocks, const GateWs& ws,
   const int nc = run;
   uint32_t tk;
   int32_t tg;
-  int bits = 0;
-  auto closed = [&](int32_t p) {  // is the parent p of a selected node selected?
-    if (p < 0) return true;
-    const uint32_t kp = ws.keys[p];
-    return kp != 0u && (kp > tk || (kp == tk && p <= tg));
-  };
+  // No ancestor-closure check is needed: a child's score is its parent's plus a
+  // clamped log q <= 0 in one binary32 add, so the parent's key is at least the
+  // child's, and its global index is smaller; under (key descending, index
+  // ascending) the parent of a selected node is always selected.
+  (void)status;
   if (nc <= kSortCap && nblocks <= kGateThreads) {
     if (threadIdx.x == 0) s_base[nblocks] = nc;
     __syncthreads();
@@ -251,7 +250,6 @@ __device__ void gate_finish_body(int N, int nblocks, const GateWs& ws,
       const int32_t g = s_g[i];
       const bool sel = k > tk || (k == tk && g <= tg);
       selected[g] = sel ? 1 : 0;
-      if (sel && !closed(ws.pglob[g])) bits |= ECHO_DATA_NOT_CLOSED;
     }
   } else {
     __syncthreads();
@@ -264,7 +262,6 @@ __device__ void gate_finish_body(int N, int nblocks, const GateWs& ws,
         const uint2 e = ws.cand[size_t(b) * kGateThreads + i];
         const bool sel = e.x > tk || (e.x == tk && int32_t(e.y) <= tg);
         selected[e.y] = sel ? 1 : 0;
-        if (sel && !closed(ws.pglob[e.y])) bits |= ECHO_DATA_NOT_CLOSED;
       }
     }
   }
@@ -272,7 +269,6 @@ __device__ void gate_finish_body(int N, int nblocks, const GateWs& ws,
     ws.meta->thr_key = tk;
     ws.meta->thr_g = tg;
   }
-  wave_status_or(status, bits);
 }
 
 
