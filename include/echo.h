@@ -76,9 +76,9 @@ typedef void* echo_stream_t; /* hipStream_t */
  * (eq. 4 budget; Theorem 2 / Proposition 1 exchange argument): the
  * min(budget, #finite S) candidates of the whole batch with the largest S;
  * ties go to the smaller global candidate index; S = -inf is never selected.
- * Because log q <= 0 the selection is closed under parents; a parallel pass
- * checks every selected node's parent and sets ECHO_DATA_NOT_CLOSED if one is
- * missing (impossible for data that passed the clamps below).
+ * Because log q <= 0 (after the clamps below) a parent's S is at least its
+ * child's and its index is smaller, so the selection is closed under parents
+ * by construction; this call never sets ECHO_DATA_NOT_CLOSED.
  *
  *   cand_offsets [R+1] int32   request-major CSR of candidates; g = cand_offsets[r] + n
  *   parent       [N]   int32   request-local parent index, -1 = child of the root;
